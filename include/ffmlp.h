@@ -1,0 +1,164 @@
+/*
+ * ffmlp: fully-fused narrow MLPs on AMD Instinct MI355X (gfx950).
+ *
+ * C ABI of the library.  The operations are those of "Fully-fused
+ * Multi-Layer Perceptrons on Intel Data Center GPUs" (arXiv 2403.17607),
+ * section III-A:
+ *   - inference, Algorithm 1: A_1 = X, C_i = A_i B_i, A_{i+1} = sigma(C_i);
+ *   - the training step, Algorithm 2: the forward pass keeping every A_i,
+ *     the L2 loss, the output delta, backward propagation of the deltas
+ *     D_i = sigma_b(A_i, D_{i+1} B_i^T) down to i = 2 (no input gradient),
+ *     and the weight gradients G_i = A_i^T D_{i+1}.  No optimizer step
+ *     (the paper leaves it out of the algorithm).
+ * Weights B_i are stored fan_in x fan_out and used as C = A B (section
+ * III-A); there are no bias terms (the algorithms have none).
+ *
+ * Shapes.  An MLP has `depth` hidden layers of `width` neurons, i.e.
+ * L = depth + 1 weight matrices: in_dim x width, (depth - 1) times
+ * width x width, width x out_dim (for depth = 0: one in_dim x out_dim
+ * matrix).  width is 16, 32, 64 or 128 (section I); 1 <= in_dim, out_dim
+ * <= width.  Smaller input and output widths are reduced to the square case
+ * by zero padding inside the library (section III-A).
+ *
+ * Precision.  All matrix products take bf16 operands and accumulate in fp32
+ * (section III-B).  Every activation, delta and output stored is rounded
+ * once to bf16, round-to-nearest-even; weight gradients are fp32.
+ *
+ * Memory.  Every pointer argument except `mlp_t*`, `fan_in`, `fan_out` and
+ * `offset` of mlp_layer_shape is DEVICE memory on the current HIP device,
+ * owned by the caller.  The library never allocates device memory, never
+ * synchronizes the stream and keeps no device state: a handle holds host
+ * metadata only and is immutable after mlp_set_output_activation, so one
+ * handle may be used from several streams at once as long as each call has
+ * its own workspace.  Calls that share a workspace on overlapping streams
+ * race.  All work is enqueued on `stream` (a hipStream_t; NULL means the
+ * default stream).
+ *
+ * Errors.  Every int-returning call returns MLP_OK (0) or a negative code.
+ * Argument errors are detected on the host before anything is enqueued;
+ * mlp_last_error() (thread-local) then describes the problem.  Faults of
+ * enqueued kernels surface at the caller's next synchronization.
+ */
+#ifndef FFMLP_H
+#define FFMLP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef struct mlp mlp_t;
+
+/* Activations (section III-A uses ReLU hidden layers with a linear output
+ * in its benchmarks; sigmoid and sine serve the application-shaped nets). */
+enum {
+  MLP_ACT_LINEAR = 0,
+  MLP_ACT_RELU = 1,
+  MLP_ACT_SIGMOID = 2, /* 1 / (1 + exp(-x)) */
+  MLP_ACT_SINE = 3     /* sin(x) */
+};
+
+enum {
+  MLP_OK = 0,
+  MLP_ERR_INVALID_ARG = -1, /* null pointer, bad size, misaligned pointer */
+  MLP_ERR_UNSUPPORTED = -2, /* width not in {16, 32, 64, 128}, bad activation */
+  MLP_ERR_WORKSPACE = -3,   /* workspace smaller than mlp_workspace_bytes */
+  MLP_ERR_HIP = -4          /* a HIP runtime call or launch failed */
+};
+
+enum { MLP_MODE_INFER = 0, MLP_MODE_TRAIN = 1 };
+
+/* Create a handle (host memory only).  `activation` applies to the hidden
+ * layers; the output activation defaults to linear.  Returns
+ * MLP_ERR_UNSUPPORTED for a width outside {16, 32, 64, 128} or an unknown
+ * activation, MLP_ERR_INVALID_ARG for depth < 0, in_dim or out_dim outside
+ * [1, width], or out == NULL. */
+int mlp_create(int width, int depth, int in_dim, int out_dim, int activation,
+               mlp_t** out);
+
+/* Set the activation of the output layer (default MLP_ACT_LINEAR). */
+int mlp_set_output_activation(mlp_t* h, int activation);
+
+/* Free the handle.  NULL is ignored. */
+void mlp_destroy(mlp_t* h);
+
+/* Number of weights, sum over layers of fan_in * fan_out (real dims). */
+int64_t mlp_param_count(const mlp_t* h);
+
+/* Real shape of weight matrix l (0-based, 0 <= l <= depth) and its offset,
+ * in elements, inside the concatenated weight and gradient buffers.  Any of
+ * the three output pointers may be NULL. */
+int mlp_layer_shape(const mlp_t* h, int l, int* fan_in, int* fan_out,
+                    int64_t* offset);
+
+/* Bytes of the packed-weight buffer written by mlp_pack_weights. */
+size_t mlp_packed_bytes(const mlp_t* h);
+
+/* Rearrange the weights into the operand order of the matrix cores, zero
+ * padded, in the two orientations the forward and backward passes use (the
+ * counterpart of the packed format of section III-B).
+ *   W       bf16 bit patterns, mlp_param_count(h) elements: the L matrices
+ *           concatenated, each row-major [fan_in][fan_out].  2-byte aligned.
+ *   packed  mlp_packed_bytes(h) bytes, 16-byte aligned, written in full.
+ * Call it again after every weight update. */
+int mlp_pack_weights(const mlp_t* h, const uint16_t* W, void* packed,
+                     void* stream);
+
+/* Workspace bytes for a batch of M rows.  MLP_MODE_INFER: 0 (inference
+ * needs none).  MLP_MODE_TRAIN: the activation stash, the deltas and the
+ * per-workgroup partial sums used by mlp_forward (with a stash),
+ * mlp_backward and mlp_train_step.  Depends only on the handle and M. */
+size_t mlp_workspace_bytes(const mlp_t* h, int64_t M, int mode);
+
+/*
+ * Forward pass, Algorithm 1.
+ *   X      bf16 [M][in_dim], row-major, contiguous, 16-byte aligned.
+ *   Y      bf16 [M][out_dim], row-major, contiguous, 8-byte aligned.
+ *   stash  NULL for inference.  Otherwise a training workspace of at least
+ *          mlp_workspace_bytes(h, M, MLP_MODE_TRAIN) bytes, 256-byte
+ *          aligned: the forward pass of Algorithm 2 then also keeps every
+ *          hidden activation there for a later mlp_backward.
+ * M >= 0 rows (M = 0 enqueues nothing).
+ */
+int mlp_forward(const mlp_t* h, const void* packed, const uint16_t* X,
+                uint16_t* Y, int64_t M, void* stash, void* stream);
+
+/*
+ * Backward pass of Algorithm 2 seeded with dY = dLoss/dY, after
+ * mlp_forward(..., stash = ws) on the same X, M and packed weights.
+ *   X   the forward's input (needed for G_1 = A_1^T D_2).
+ *   dY  fp32 [M][out_dim], row-major, 16-byte aligned.
+ *   G   fp32, mlp_param_count(h) elements, same layout as the weights;
+ *       overwritten with the weight gradients.  No input gradient.
+ *   ws  the workspace the forward pass stashed into.
+ */
+int mlp_backward(const mlp_t* h, const void* packed, const uint16_t* X,
+                 const float* dY, float* G, int64_t M, void* ws,
+                 void* stream);
+
+/*
+ * One training step, Algorithm 2: forward with stash, mean-squared-error
+ * loss over the M * out_dim outputs, output delta 2 (Y - T) / (M out_dim)
+ * times the output activation's derivative, backward propagation and the
+ * weight gradients.  No optimizer step.
+ *   T     fp32 targets [M][out_dim], row-major, 16-byte aligned.
+ *   Y     optional bf16 output [M][out_dim] (NULL: not stored).
+ *   G     fp32 gradients, mlp_param_count(h) elements (overwritten).
+ *   loss  optional device float, set to sum (Y - T)^2 / (M out_dim)
+ *         computed from the fp32 outputs before rounding.
+ *   ws    mlp_workspace_bytes(h, M, MLP_MODE_TRAIN) bytes, 256-byte aligned.
+ */
+int mlp_train_step(const mlp_t* h, const void* packed, const uint16_t* X,
+                   const float* T, uint16_t* Y, float* G, float* loss,
+                   int64_t M, void* ws, void* stream);
+
+/* Description of the last error on this thread ("" if none). */
+const char* mlp_last_error(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif

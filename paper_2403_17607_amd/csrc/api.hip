@@ -1,0 +1,418 @@
+// C ABI of the library (include/ffmlp.h): argument checks, workspace
+// layout and the launch sequence of each entry point.  Host code only.
+#include <hip/hip_runtime.h>
+
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <mutex>
+#include <string>
+#include <vector>
+
+#include "common.h"
+#include "ffmlp.h"
+
+using namespace ffmlp;
+
+struct mlp {
+  int width, depth, in_dim, out_dim, act, out_act;
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+int fail(int code, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+int fail(int code, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return code;
+}
+
+int hip_fail(hipError_t e, const char* what) {
+  return fail(MLP_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool aligned(const void* p, size_t a) { return (reinterpret_cast<uintptr_t>(p) % a) == 0; }
+
+size_t round_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+int n_mats(const mlp* h) { return h->depth + 1; }
+int fan_in_of(const mlp* h, int l) { return l == 0 ? h->in_dim : h->width; }
+int fan_out_of(const mlp* h, int l) { return l == n_mats(h) - 1 ? h->out_dim : h->width; }
+int kblocks(int n) { return (n + 31) / 32; }
+int strips(int n) { return (n + 15) / 16; }
+
+// Fragment counts of the packed buffer: forward layers 0 .. L-1, then
+// backward layers 1 .. L-1.
+struct PackGeom {
+  uint32_t fwd_frag[2], fwd_total;  // [0] = layer 0, [1] = hidden layers
+  uint32_t bwd_hidden, bwd_total;
+};
+
+PackGeom pack_geom(const mlp* h) {
+  const int W = h->width, L = n_mats(h);
+  PackGeom g{};
+  uint32_t total = 0;
+  for (int l = 0; l < L; ++l) {
+    const uint32_t f = (uint32_t)strips(fan_out_of(h, l)) * kblocks(fan_in_of(h, l));
+    if (l == 0) g.fwd_frag[0] = f;
+    if (l == 1) g.fwd_frag[1] = f;
+    total += f;
+  }
+  g.fwd_total = total;
+  g.fwd_frag[1] = (uint32_t)strips(W) * kblocks(W);
+  uint32_t bt = 0;
+  for (int l = 1; l < L; ++l) bt += (uint32_t)strips(fan_in_of(h, l)) * kblocks(fan_out_of(h, l));
+  g.bwd_hidden = (uint32_t)strips(W) * kblocks(W);
+  g.bwd_total = bt;
+  return g;
+}
+
+// Workspace layout for a batch of M rows (byte offsets, 256-byte aligned).
+struct WsLayout {
+  int64_t M16;
+  size_t stashA, stashS, deltaH, deltaOut, cOut, partial, lossPart, total;
+  int P, chunks_per_block;
+};
+
+WsLayout ws_layout(const mlp* h, int64_t M) {
+  WsLayout w{};
+  const int W = h->width, L = n_mats(h);
+  const int OP = strips(h->out_dim) * 16;
+  w.M16 = (M + 15) / 16 * 16;
+  const size_t hid = (size_t)(L - 1) * w.M16 * W * 2;
+  size_t o = 0;
+  w.stashA = o; o = round_up(o + hid, 256);
+  w.stashS = o; o = round_up(o + (h->act == MLP_ACT_SINE ? hid : 0), 256);
+  w.deltaH = o; o = round_up(o + hid, 256);
+  w.deltaOut = o; o = round_up(o + (size_t)w.M16 * OP * 2, 256);
+  w.cOut = o; o = round_up(o + (h->out_act != MLP_ACT_LINEAR ? (size_t)w.M16 * OP * 4 : 0), 256);
+  const int CH = wgrad_chunk(W);
+  const int64_t nch = (M + CH - 1) / CH;
+  int64_t P = (kWgradTargetBlocks + L - 1) / L;
+  if (P > nch) P = nch;
+  if (P < 1) P = 1;
+  const int64_t cpb = nch > 0 ? (nch + P - 1) / P : 0;
+  P = cpb > 0 ? (nch + cpb - 1) / cpb : 1;  // no empty workgroups
+  w.P = (int)P;
+  w.chunks_per_block = (int)cpb;
+  int64_t params = 0;
+  for (int l = 0; l < L; ++l) params += (int64_t)fan_in_of(h, l) * fan_out_of(h, l);
+  w.partial = o; o = round_up(o + (size_t)P * params * 4, 256);
+  w.lossPart = o; o = round_up(o + (size_t)kMaxLossParts * 4, 256);
+  w.total = o;
+  return w;
+}
+
+int64_t param_count(const mlp* h) {
+  int64_t p = 0;
+  for (int l = 0; l < n_mats(h); ++l) p += (int64_t)fan_in_of(h, l) * fan_out_of(h, l);
+  return p;
+}
+
+bool valid_act(int a) { return a >= MLP_ACT_LINEAR && a <= MLP_ACT_SINE; }
+
+int check_handle(const mlp* h) {
+  if (!h) return fail(MLP_ERR_INVALID_ARG, "null handle");
+  return MLP_OK;
+}
+
+FwdArgs fwd_args(const mlp* h, const void* packed, const uint16_t* X, int64_t M) {
+  const PackGeom g = pack_geom(h);
+  FwdArgs a{};
+  a.packed = static_cast<const u32x4*>(packed);
+  a.X = X;
+  a.M = M;
+  a.M16 = (M + 15) / 16 * 16;
+  a.in_dim = h->in_dim;
+  a.out_dim = h->out_dim;
+  a.L = n_mats(h);
+  a.out_act = h->out_act;
+  a.scale = M > 0 ? (float)(2.0 / ((double)M * h->out_dim)) : 0.f;
+  const int64_t rows = tile_rows(h->width);
+  a.ntiles = (int)((M + rows - 1) / rows);
+  a.lay0_frags = g.fwd_frag[0];
+  a.layH_frags = g.fwd_frag[1];
+  a.total_frags = g.fwd_total;
+  return a;
+}
+
+BwdArgs bwd_args(const mlp* h, const void* packed, const WsLayout& w, uint8_t* ws, int64_t M) {
+  const PackGeom g = pack_geom(h);
+  BwdArgs b{};
+  b.packed = reinterpret_cast<const u32x4*>(static_cast<const uint8_t*>(packed) + (size_t)g.fwd_total * 1024);
+  b.stashA = reinterpret_cast<const uint16_t*>(ws + w.stashA);
+  b.stashS = h->act == MLP_ACT_SINE ? reinterpret_cast<const uint16_t*>(ws + w.stashS) : nullptr;
+  b.deltaH = reinterpret_cast<uint16_t*>(ws + w.deltaH);
+  b.deltaOut = reinterpret_cast<uint16_t*>(ws + w.deltaOut);
+  b.cOut = h->out_act != MLP_ACT_LINEAR ? reinterpret_cast<const float*>(ws + w.cOut) : nullptr;
+  b.M = M;
+  b.M16 = w.M16;
+  b.out_dim = h->out_dim;
+  b.L = n_mats(h);
+  b.out_act = h->out_act;
+  const int64_t rows = tile_rows(h->width);
+  b.ntiles = (int)((M + rows - 1) / rows);
+  b.layH_frags = g.bwd_hidden;
+  b.total_frags = g.bwd_total;
+  return b;
+}
+
+int run_wgrad_reduce(const mlp* h, const uint16_t* X, const WsLayout& w, uint8_t* ws, int64_t M,
+                     float* G, float* loss, int nloss, hipStream_t s) {
+  const int64_t params = param_count(h);
+  if (M > 0) {
+    WgradArgs a{};
+    a.X = X;
+    a.stashA = reinterpret_cast<const uint16_t*>(ws + w.stashA);
+    a.deltaH = reinterpret_cast<const uint16_t*>(ws + w.deltaH);
+    a.deltaOut = reinterpret_cast<const uint16_t*>(ws + w.deltaOut);
+    a.partial = reinterpret_cast<float*>(ws + w.partial);
+    a.M = M;
+    a.M16 = w.M16;
+    a.params = params;
+    a.in_dim = h->in_dim;
+    a.out_dim = h->out_dim;
+    a.L = n_mats(h);
+    a.P = w.P;
+    a.chunks_per_block = w.chunks_per_block;
+    hipError_t e = launch_wgrad(h->width, a, s);
+    if (e != hipSuccess) return hip_fail(e, "weight-gradient kernel launch");
+  }
+  ReduceArgs r{};
+  r.partial = reinterpret_cast<const float*>(ws + w.partial);
+  r.G = G;
+  r.params = params;
+  r.P = M > 0 ? w.P : 0;
+  r.lossPart = reinterpret_cast<const float*>(ws + w.lossPart);
+  r.nloss = M > 0 ? nloss : 0;
+  r.loss = loss;
+  r.loss_scale = M > 0 ? (float)(1.0 / ((double)M * h->out_dim)) : 0.f;
+  hipError_t e = launch_reduce(r, s);
+  if (e != hipSuccess) return hip_fail(e, "reduce kernel launch");
+  return MLP_OK;
+}
+
+}  // namespace
+
+namespace ffmlp {
+
+hipError_t device_info(DeviceInfo* out) {
+  static std::mutex mu;
+  static std::vector<DeviceInfo> cache;
+  static std::vector<char> have;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)cache.size() <= dev) {
+    cache.resize(dev + 1);
+    have.resize(dev + 1, 0);
+  }
+  if (!have[dev]) {
+    DeviceInfo d{};
+    e = hipDeviceGetAttribute(&d.cus, hipDeviceAttributeMultiprocessorCount, dev);
+    if (e != hipSuccess) return e;
+    e = hipDeviceGetAttribute(&d.max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, dev);
+    if (e != hipSuccess) return e;
+    cache[dev] = d;
+    have[dev] = 1;
+  }
+  *out = cache[dev];
+  return hipSuccess;
+}
+
+}  // namespace ffmlp
+
+extern "C" {
+
+const char* mlp_last_error(void) { return g_err.c_str(); }
+
+int mlp_create(int width, int depth, int in_dim, int out_dim, int activation, mlp_t** out) {
+  g_err.clear();
+  if (!out) return fail(MLP_ERR_INVALID_ARG, "out is NULL");
+  *out = nullptr;
+  if (width != 16 && width != 32 && width != 64 && width != 128)
+    return fail(MLP_ERR_UNSUPPORTED, "width %d is not one of 16, 32, 64, 128", width);
+  if (!valid_act(activation)) return fail(MLP_ERR_UNSUPPORTED, "unknown activation %d", activation);
+  if (depth < 0) return fail(MLP_ERR_INVALID_ARG, "depth %d < 0", depth);
+  if (in_dim < 1 || in_dim > width)
+    return fail(MLP_ERR_INVALID_ARG, "in_dim %d outside [1, %d]", in_dim, width);
+  if (out_dim < 1 || out_dim > width)
+    return fail(MLP_ERR_INVALID_ARG, "out_dim %d outside [1, %d]", out_dim, width);
+  mlp* h = new (std::nothrow) mlp{width, depth, in_dim, out_dim, activation, MLP_ACT_LINEAR};
+  if (!h) return fail(MLP_ERR_INVALID_ARG, "out of host memory");
+  *out = h;
+  return MLP_OK;
+}
+
+int mlp_set_output_activation(mlp_t* h, int activation) {
+  g_err.clear();
+  if (int rc = check_handle(h)) return rc;
+  if (!valid_act(activation)) return fail(MLP_ERR_UNSUPPORTED, "unknown activation %d", activation);
+  h->out_act = activation;
+  return MLP_OK;
+}
+
+void mlp_destroy(mlp_t* h) { delete h; }
+
+int64_t mlp_param_count(const mlp_t* h) { return h ? param_count(h) : 0; }
+
+int mlp_layer_shape(const mlp_t* h, int l, int* fan_in, int* fan_out, int64_t* offset) {
+  g_err.clear();
+  if (int rc = check_handle(h)) return rc;
+  if (l < 0 || l >= n_mats(h)) return fail(MLP_ERR_INVALID_ARG, "layer %d outside [0, %d]", l, h->depth);
+  int64_t off = 0;
+  for (int i = 0; i < l; ++i) off += (int64_t)fan_in_of(h, i) * fan_out_of(h, i);
+  if (fan_in) *fan_in = fan_in_of(h, l);
+  if (fan_out) *fan_out = fan_out_of(h, l);
+  if (offset) *offset = off;
+  return MLP_OK;
+}
+
+size_t mlp_packed_bytes(const mlp_t* h) {
+  if (!h) return 0;
+  const PackGeom g = pack_geom(h);
+  return (size_t)(g.fwd_total + g.bwd_total) * 1024;
+}
+
+int mlp_pack_weights(const mlp_t* h, const uint16_t* W, void* packed, void* stream) {
+  g_err.clear();
+  if (int rc = check_handle(h)) return rc;
+  if (!W || !packed) return fail(MLP_ERR_INVALID_ARG, "null weight or packed pointer");
+  if (!aligned(W, 2) || !aligned(packed, 16))
+    return fail(MLP_ERR_INVALID_ARG, "W must be 2-byte and packed 16-byte aligned");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const int L = n_mats(h);
+  uint16_t* dst = static_cast<uint16_t*>(packed);
+  int64_t woff = 0;
+  for (int l = 0; l < L; ++l) {
+    PackArgs a{};
+    a.W = W + woff;
+    a.fan_in = fan_in_of(h, l);
+    a.fan_out = fan_out_of(h, l);
+    a.strips = strips(a.fan_out);
+    a.kblocks = kblocks(a.fan_in);
+    a.dir = 0;
+    a.first = l == 0;
+    a.dst = dst;
+    hipError_t e = launch_pack(a, s);
+    if (e != hipSuccess) return hip_fail(e, "pack kernel launch");
+    dst += (size_t)a.strips * a.kblocks * 512;
+    woff += (int64_t)a.fan_in * a.fan_out;
+  }
+  woff = (int64_t)fan_in_of(h, 0) * fan_out_of(h, 0);
+  for (int l = 1; l < L; ++l) {
+    PackArgs a{};
+    a.W = W + woff;
+    a.fan_in = fan_in_of(h, l);
+    a.fan_out = fan_out_of(h, l);
+    a.strips = strips(a.fan_in);
+    a.kblocks = kblocks(a.fan_out);
+    a.dir = 1;
+    a.first = 0;
+    a.dst = dst;
+    hipError_t e = launch_pack(a, s);
+    if (e != hipSuccess) return hip_fail(e, "pack kernel launch");
+    dst += (size_t)a.strips * a.kblocks * 512;
+    woff += (int64_t)a.fan_in * a.fan_out;
+  }
+  return MLP_OK;
+}
+
+size_t mlp_workspace_bytes(const mlp_t* h, int64_t M, int mode) {
+  if (!h || M < 0 || mode != MLP_MODE_TRAIN) return 0;
+  return ws_layout(h, M).total;
+}
+
+int mlp_forward(const mlp_t* h, const void* packed, const uint16_t* X, uint16_t* Y, int64_t M,
+                void* stash, void* stream) {
+  g_err.clear();
+  if (int rc = check_handle(h)) return rc;
+  if (M < 0) return fail(MLP_ERR_INVALID_ARG, "M = %lld < 0", (long long)M);
+  if (M == 0) return MLP_OK;
+  if (!packed || !X || !Y) return fail(MLP_ERR_INVALID_ARG, "null packed, X or Y");
+  if (!aligned(packed, 16) || !aligned(X, 16) || !aligned(Y, 8))
+    return fail(MLP_ERR_INVALID_ARG, "packed and X must be 16-byte, Y 8-byte aligned");
+  if (stash && !aligned(stash, 256)) return fail(MLP_ERR_INVALID_ARG, "stash must be 256-byte aligned");
+  if (M > ((int64_t)1 << 36)) return fail(MLP_ERR_INVALID_ARG, "M > 2^36");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  FwdArgs a = fwd_args(h, packed, X, M);
+  a.Y = Y;
+  int mode = FWD_INFER;
+  if (stash) {
+    const WsLayout w = ws_layout(h, M);
+    uint8_t* ws = static_cast<uint8_t*>(stash);
+    a.stashA = reinterpret_cast<uint16_t*>(ws + w.stashA);
+    a.stashS = h->act == MLP_ACT_SINE ? reinterpret_cast<uint16_t*>(ws + w.stashS) : nullptr;
+    a.cOut = h->out_act != MLP_ACT_LINEAR ? reinterpret_cast<float*>(ws + w.cOut) : nullptr;
+    mode = FWD_STASH;
+  }
+  hipError_t e = launch_forward(h->width, h->act, mode, a, s, nullptr);
+  if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
+  return MLP_OK;
+}
+
+int mlp_backward(const mlp_t* h, const void* packed, const uint16_t* X, const float* dY, float* G,
+                 int64_t M, void* ws_, void* stream) {
+  g_err.clear();
+  if (int rc = check_handle(h)) return rc;
+  if (M < 0) return fail(MLP_ERR_INVALID_ARG, "M = %lld < 0", (long long)M);
+  if (!G || !ws_) return fail(MLP_ERR_INVALID_ARG, "null G or workspace");
+  if (M > 0 && (!packed || !X || !dY)) return fail(MLP_ERR_INVALID_ARG, "null packed, X or dY");
+  if (!aligned(G, 4) || !aligned(ws_, 256) || (M > 0 && (!aligned(packed, 16) || !aligned(X, 16) || !aligned(dY, 16))))
+    return fail(MLP_ERR_INVALID_ARG, "misaligned pointer (packed, X, dY: 16 bytes; ws: 256; G: 4)");
+  if (M > ((int64_t)1 << 36)) return fail(MLP_ERR_INVALID_ARG, "M > 2^36");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const WsLayout w = ws_layout(h, M);
+  uint8_t* ws = static_cast<uint8_t*>(ws_);
+  if (M > 0) {
+    BwdArgs b = bwd_args(h, packed, w, ws, M);
+    b.dY = dY;
+    hipError_t e = launch_backward(h->width, h->act, 1, b, s);
+    if (e != hipSuccess) return hip_fail(e, "backward kernel launch");
+  }
+  return run_wgrad_reduce(h, X, w, ws, M, G, nullptr, 0, s);
+}
+
+int mlp_train_step(const mlp_t* h, const void* packed, const uint16_t* X, const float* T,
+                   uint16_t* Y, float* G, float* loss, int64_t M, void* ws_, void* stream) {
+  g_err.clear();
+  if (int rc = check_handle(h)) return rc;
+  if (M < 0) return fail(MLP_ERR_INVALID_ARG, "M = %lld < 0", (long long)M);
+  if (!G || !ws_) return fail(MLP_ERR_INVALID_ARG, "null G or workspace");
+  if (M > 0 && (!packed || !X || !T)) return fail(MLP_ERR_INVALID_ARG, "null packed, X or T");
+  if (!aligned(G, 4) || !aligned(ws_, 256) || (loss && !aligned(loss, 4)) ||
+      (M > 0 && (!aligned(packed, 16) || !aligned(X, 16) || !aligned(T, 16) || (Y && !aligned(Y, 8)))))
+    return fail(MLP_ERR_INVALID_ARG,
+                "misaligned pointer (packed, X, T: 16 bytes; Y: 8; ws: 256; G, loss: 4)");
+  if (M > ((int64_t)1 << 36)) return fail(MLP_ERR_INVALID_ARG, "M > 2^36");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  const WsLayout w = ws_layout(h, M);
+  uint8_t* ws = static_cast<uint8_t*>(ws_);
+  int nloss = 0;
+  if (M > 0) {
+    FwdArgs a = fwd_args(h, packed, X, M);
+    a.Y = Y;
+    a.T = T;
+    a.stashA = reinterpret_cast<uint16_t*>(ws + w.stashA);
+    a.stashS = h->act == MLP_ACT_SINE ? reinterpret_cast<uint16_t*>(ws + w.stashS) : nullptr;
+    a.deltaOut = reinterpret_cast<uint16_t*>(ws + w.deltaOut);
+    a.lossPart = reinterpret_cast<float*>(ws + w.lossPart);
+    hipError_t e = launch_forward(h->width, h->act, FWD_TRAIN, a, s, &nloss);
+    if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
+    if (n_mats(h) > 1) {
+      BwdArgs b = bwd_args(h, packed, w, ws, M);
+      e = launch_backward(h->width, h->act, 0, b, s);
+      if (e != hipSuccess) return hip_fail(e, "backward kernel launch");
+    }
+  }
+  return run_wgrad_reduce(h, X, w, ws, M, G, loss, nloss, s);
+}
+
+}  // extern "C"

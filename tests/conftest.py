@@ -22,9 +22,19 @@ def gpu_available() -> bool:
 
 
 @pytest.fixture(scope="session")
-def gpu():
-    """Skip-free GPU guard: a test marked gpu that runs without a GPU is an
-    error, not a silent pass."""
+def ffmlp():
+    """The GPU package with its library loaded; built here only if absent."""
+    import paper_2403_17607_amd as pkg
+    if not os.path.exists(pkg.LIB_PATH):
+        from paper_2403_17607_amd import build
+        build.build()
+    pkg.lib()
+    return pkg
+
+
+@pytest.fixture(scope="session")
+def gpu(ffmlp):
+    """A GPU test that runs without a GPU is an error, not a silent pass."""
     if not gpu_available():
         pytest.fail("this test needs a GPU (run with -m 'not gpu' on a CPU host)")
     import torch

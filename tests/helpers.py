@@ -1,0 +1,63 @@
+"""Shared pieces of the parity tests: seeded inputs (from datagen), the
+oracle's view of a net, and the two error measures with their bounds.
+
+Bounds (per output and per weight-gradient matrix):
+  outputs    max_i |Y_i - Yref_i| / max(|Yref_i|, rms(Yref)) <= 2e-2
+  gradients  ||G_l - Gref_l||_F / ||Gref_l||_F <= 1e-2
+The GPU rounds to bf16 at the same points as the oracle; what differs is
+the fp32 (GPU) versus fp64 (oracle) accumulation, which can move a value
+across a bf16 rounding boundary (one bf16 ulp = 2^-8 relative) and those
+flips propagate through later layers.
+"""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import datagen
+import oracle
+
+OUT_TOL = 2e-2
+GRAD_TOL = 1e-2
+LOSS_TOL = 1e-3
+
+ACT = {"linear": 0, "relu": 1, "sigmoid": 2, "sine": 3}
+
+
+def inputs(seed, width, depth, in_dim, out_dim, M, t_range=(-1.0, 1.0)):
+    """bf16 weights, bf16 X and fp32 T on the CPU (datagen recipes)."""
+    W = datagen.xavier_weights(seed, width, depth, in_dim, out_dim)
+    X = datagen.inputs_uniform(seed, M, in_dim)
+    T = datagen.targets_uniform(seed, M, out_dim, *t_range)
+    return W, X, T
+
+
+def oracle_net(width, depth, in_dim, out_dim, act="relu", out_act="linear"):
+    return oracle.Net(width, depth, in_dim, out_dim, ACT[act], ACT[out_act])
+
+
+def f64(t):
+    return t.detach().to("cpu").to(torch.float64).numpy()
+
+
+def out_err(Y, Yref) -> float:
+    Y, Yref = np.asarray(Y, np.float64), np.asarray(Yref, np.float64)
+    if Yref.size == 0:
+        return 0.0
+    rms = float(np.sqrt(np.mean(Yref ** 2)))
+    denom = np.maximum(np.abs(Yref), rms if rms > 0 else 1.0)
+    return float(np.max(np.abs(Y - Yref) / denom))
+
+
+def grad_errs(G, Gref, net) -> list[float]:
+    """Relative Frobenius error of every layer's gradient."""
+    G, Gref = np.asarray(G, np.float64), np.asarray(Gref, np.float64)
+    errs = []
+    total = np.linalg.norm(Gref) or 1.0
+    for g, r in zip(net.split(G), net.split(Gref)):
+        nr = np.linalg.norm(r)
+        if nr < 1e-12 * total:
+            errs.append(float(np.linalg.norm(g - r) / total))
+        else:
+            errs.append(float(np.linalg.norm(g - r) / nr))
+    return errs

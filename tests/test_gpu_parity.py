@@ -1,0 +1,252 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Every case draws seeded inputs with datagen, runs the library on the GPU and
+the oracle on the CPU on the same values, and compares element by element
+with the bounds stated in helpers.py.  Bitwise properties (identity
+weights, power-of-two scaling, row permutation, run-to-run determinism) are
+checked exactly.
+"""
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import datagen
+from helpers import (GRAD_TOL, LOSS_TOL, OUT_TOL, f64, grad_errs, inputs, oracle_net,
+                     out_err)
+
+pytestmark = pytest.mark.gpu
+
+
+def log(*a):
+    print(*a, flush=True)
+    sys.stdout.flush()
+
+
+def run_case(ffmlp, dev, width, depth, in_dim, out_dim, M, act="relu", out_act="linear",
+             seed=11, train=True, t_range=(-1.0, 1.0)):
+    log(f"case w={width} d={depth} in={in_dim} out={out_dim} M={M} act={act} out={out_act}")
+    W, X, T = inputs(seed, width, depth, in_dim, out_dim, M, t_range)
+    onet = oracle_net(width, depth, in_dim, out_dim, act, out_act)
+    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, act, out_act)
+    Wd, Xd, Td = W.to(dev), X.to(dev), T.to(dev)
+    packed = net.pack(Wd)
+    Y = net.forward(packed, Xd)
+    res = {"net": net, "onet": onet, "packed": packed, "W": W, "X": X, "T": T, "Y": Y}
+    if train:
+        ws = net.workspace(M, dev)
+        Yt = torch.empty_like(Y)
+        G, loss = net.train_step(packed, Xd, Td, ws, Y=Yt)
+        torch.cuda.synchronize()
+        ref = onet.train_step(W, X, T)
+        res.update(G=G, loss=loss, Yt=Yt, ref=ref, ws=ws)
+        assert out_err(f64(Y), ref["Y"]) <= OUT_TOL
+        assert torch.equal(Y, Yt), "train-step outputs differ from inference outputs"
+        errs = grad_errs(f64(G), ref["G"], onet)
+        log("  grad errs", ["%.2e" % e for e in errs])
+        assert max(errs) <= GRAD_TOL
+        lref = ref["loss"]
+        assert abs(loss.item() - lref) <= LOSS_TOL * max(abs(lref), 1e-30)
+    else:
+        torch.cuda.synchronize()
+        Yref, _ = onet.forward(W, X)
+        assert out_err(f64(Y), Yref) <= OUT_TOL
+    return res
+
+
+# ------------------------------------------------------------------ configs --
+
+def test_tiny_config(ffmlp, gpu):
+    """Input 64, 4 hidden layers of 64, ReLU, linear output 64, batch 4096."""
+    r = run_case(ffmlp, gpu, 64, 4, 64, 64, 4096, seed=1)
+    Yref = r["ref"]["Y"]
+    match = np.mean(f64(r["Y"]) == Yref)
+    log(f"  bitwise-equal outputs: {match:.4f}")
+    assert match > 0.9
+
+
+@pytest.mark.parametrize("width", [16, 32, 64, 128])
+@pytest.mark.parametrize("M", [1, 7, 4097])
+def test_width_sweep_shapes(ffmlp, gpu, width, M):
+    """The sweep shape (in = width, out 16, 4 hidden layers) at tail sizes."""
+    run_case(ffmlp, gpu, width, 4, width, 16, M, seed=2)
+
+
+@pytest.mark.parametrize("act", ["linear", "relu", "sigmoid", "sine"])
+@pytest.mark.parametrize("out_act", ["linear", "relu", "sigmoid", "sine"])
+def test_activations(ffmlp, gpu, act, out_act):
+    run_case(ffmlp, gpu, 32, 3, 29, 5, 777, act, out_act, seed=4)
+
+
+@pytest.mark.parametrize("width,depth", [(64, 0), (64, 1), (64, 2), (64, 16), (128, 16),
+                                         (16, 0), (128, 0), (32, 7)])
+def test_depths(ffmlp, gpu, width, depth):
+    run_case(ffmlp, gpu, width, depth, width, width, 1000, seed=5)
+
+
+@pytest.mark.parametrize("width,in_dim,out_dim", [(64, 1, 1), (64, 3, 3), (64, 16, 16),
+                                                  (64, 8, 1), (64, 5, 64), (128, 127, 33),
+                                                  (16, 1, 16), (32, 17, 31), (128, 40, 100)])
+def test_in_out_dims(ffmlp, gpu, width, in_dim, out_dim):
+    run_case(ffmlp, gpu, width, 2, in_dim, out_dim, 1500, seed=6)
+
+
+def test_image_like(ffmlp, gpu):
+    """Sinusoidal features of pixel coordinates, width 64, 2 hidden layers,
+    3 sigmoid outputs, targets in [0, 1]."""
+    net = ffmlp.FusedMLP(64, 2, 64, 3, "relu", "sigmoid")
+    onet = oracle_net(64, 2, 64, 3, "relu", "sigmoid")
+    M = 5000
+    X = datagen.image_features(4, M)
+    W = datagen.xavier_weights(4, 64, 2, 64, 3)
+    T = datagen.targets_uniform(4, M, 3, 0.0, 1.0)
+    packed = net.pack(W.to(gpu))
+    ws = net.workspace(M, gpu)
+    Y = torch.empty(M, 3, dtype=torch.bfloat16, device=gpu)
+    G, loss = net.train_step(packed, X.to(gpu), T.to(gpu), ws, Y=Y)
+    ref = onet.train_step(W, X, T)
+    assert out_err(f64(Y), ref["Y"]) <= OUT_TOL
+    assert max(grad_errs(f64(G), ref["G"], onet)) <= GRAD_TOL
+
+
+def test_pinn_like(ffmlp, gpu):
+    """3-D inputs, width 64, 4 sine hidden layers, one linear output."""
+    run_case(ffmlp, gpu, 64, 4, 3, 1, 3000, "sine", "linear", seed=6)
+
+
+# ---------------------------------------------------- seeded backward pass --
+
+@pytest.mark.parametrize("width,act,out_act", [(64, "relu", "linear"), (32, "sine", "sigmoid"),
+                                               (128, "sigmoid", "sine"), (16, "linear", "relu")])
+def test_forward_stash_then_backward(ffmlp, gpu, width, act, out_act):
+    depth, in_dim, out_dim, M = 3, width, 7, 2100
+    W, X, _ = inputs(7, width, depth, in_dim, out_dim, M)
+    dY = datagen.uniform(7, datagen.STREAM_AUX, (M, out_dim))
+    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, act, out_act)
+    onet = oracle_net(width, depth, in_dim, out_dim, act, out_act)
+    packed = net.pack(W.to(gpu))
+    ws = net.workspace(M, gpu)
+    Xd = X.to(gpu)
+    Y = net.forward(packed, Xd, stash=ws)
+    G = net.backward(packed, Xd, dY.to(gpu), ws)
+    Yref, _ = onet.forward(W, X)
+    Gref = onet.backward(W, X, dY)
+    assert out_err(f64(Y), Yref) <= OUT_TOL
+    assert max(grad_errs(f64(G), Gref, onet)) <= GRAD_TOL
+
+
+# ------------------------------------------------------ bitwise properties --
+
+@pytest.mark.parametrize("width", [16, 32, 64, 128])
+def test_identity_weights_bitwise(ffmlp, gpu, width):
+    """W_l = I with ReLU hidden and linear output gives Y = relu(X) exactly:
+    any mistake in the operand layouts or the chain order scrambles it."""
+    depth, M = 3, 999
+    net = ffmlp.FusedMLP(width, depth, width, width, "relu")
+    W = torch.eye(width, dtype=torch.bfloat16).flatten().repeat(depth + 1)
+    X = datagen.inputs_uniform(8, M, width)
+    Y = net.forward(net.pack(W.to(gpu)), X.to(gpu))
+    assert torch.equal(Y.cpu(), torch.relu(X))
+
+
+@pytest.mark.parametrize("width", [16, 128])
+def test_power_of_two_homogeneity_bitwise(ffmlp, gpu, width):
+    net = ffmlp.FusedMLP(width, 3, width, 16, "relu")
+    W, X, _ = inputs(9, width, 3, width, 16, 3000)
+    packed = net.pack(W.to(gpu))
+    Xd = X.to(gpu)
+    Y1 = net.forward(packed, Xd)
+    Y2 = net.forward(packed, Xd * 4)
+    assert torch.equal(Y2, Y1 * 4)
+
+
+def test_row_permutation_bitwise(ffmlp, gpu):
+    net = ffmlp.FusedMLP(64, 4, 64, 16, "sigmoid")
+    W, X, _ = inputs(10, 64, 4, 64, 16, 5000)
+    packed = net.pack(W.to(gpu))
+    perm = torch.randperm(5000, generator=torch.Generator().manual_seed(0))
+    Y = net.forward(packed, X.to(gpu))
+    Yp = net.forward(packed, X[perm].contiguous().to(gpu))
+    assert torch.equal(Yp, Y[perm.to(gpu)])
+
+
+def test_gradients_deterministic(ffmlp, gpu):
+    net = ffmlp.FusedMLP(128, 4, 128, 16, "relu")
+    M = 70000
+    W, X, T = inputs(12, 128, 4, 128, 16, M)
+    packed = net.pack(W.to(gpu))
+    ws = net.workspace(M, gpu)
+    Xd, Td = X.to(gpu), T.to(gpu)
+    G1, l1 = net.train_step(packed, Xd, Td, ws)
+    G1, l1 = G1.clone(), l1.clone()
+    G2, l2 = net.train_step(packed, Xd, Td, ws)
+    assert torch.equal(G1, G2) and torch.equal(l1, l2)
+
+
+def test_empty_batch(ffmlp, gpu):
+    net = ffmlp.FusedMLP(32, 2, 32, 16, "relu")
+    W, _, _ = inputs(13, 32, 2, 32, 16, 1)
+    packed = net.pack(W.to(gpu))
+    X = torch.empty(0, 32, dtype=torch.bfloat16, device=gpu)
+    T = torch.empty(0, 16, dtype=torch.float32, device=gpu)
+    ws = net.workspace(0, gpu)
+    G = torch.full((net.param_count(),), 7.0, device=gpu)
+    G, loss = net.train_step(packed, X, T, ws, G=G)
+    assert torch.count_nonzero(G).item() == 0 and loss.item() == 0.0
+    assert net.forward(packed, X).shape == (0, 16)
+
+
+# ------------------------------------------- full sizes, sampled rows only --
+
+def sampled_rows(M, n, seed):
+    g = torch.Generator().manual_seed(seed)
+    return torch.unique(torch.randint(0, M, (n,), generator=g))
+
+
+@pytest.mark.parametrize("width,depth,in_dim,out_dim,M", [
+    (128, 4, 128, 16, 1 << 20),       # width sweep at 2^20
+    (64, 4, 64, 16, (1 << 20) + 37),  # ragged tail
+    (32, 4, 32, 16, 1 << 20),
+    (16, 4, 16, 16, 1 << 22),         # width sweep at 2^22
+    (128, 16, 128, 128, 1 << 20),     # depth/width stress: weights stream through LDS
+])
+def test_full_size_sampled(ffmlp, gpu, width, depth, in_dim, out_dim, M):
+    """At benchmark sizes: Y on sampled rows against the oracle, and G from
+    mlp_backward with dY nonzero only on the sampled rows (G is a sum over
+    rows, so the oracle needs only those rows)."""
+    log(f"full-size w={width} d={depth} M={M}")
+    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, "relu")
+    onet = oracle_net(width, depth, in_dim, out_dim, "relu")
+    W = datagen.xavier_weights(14, width, depth, in_dim, out_dim)
+    Xd = datagen.inputs_uniform(14, M, in_dim, device=gpu)
+    rows = sampled_rows(M, 2048, 14)
+    # the same rows drawn on the CPU must be the same bits
+    Xs = torch.stack([datagen.uniform(14, datagen.STREAM_X, (in_dim,), device="cpu",
+                                      start=int(r) * in_dim) for r in rows]).to(torch.bfloat16)
+    assert torch.equal(Xs, Xd[rows.to(gpu)].cpu())
+    packed = net.pack(W.to(gpu))
+    ws = net.workspace(M, gpu)
+    Y = net.forward(packed, Xd, stash=ws)
+    dYs = datagen.uniform(14, datagen.STREAM_AUX, (len(rows), out_dim))
+    dY = torch.zeros(M, out_dim, dtype=torch.float32, device=gpu)
+    dY[rows.to(gpu)] = dYs.to(gpu)
+    G = net.backward(packed, Xd, dY, ws)
+    Yref, _ = onet.forward(W, Xs)
+    assert out_err(f64(Y[rows.to(gpu)]), Yref) <= OUT_TOL
+    Gref = onet.backward(W, Xs, dYs)
+    errs = grad_errs(f64(G), Gref, onet)
+    log("  grad errs", ["%.2e" % e for e in errs])
+    assert max(errs) <= GRAD_TOL
+    del ws
+    torch.cuda.empty_cache()
+
+
+def test_argument_errors_on_device(ffmlp, gpu):
+    net = ffmlp.FusedMLP(64, 2, 64, 16, "relu")
+    W, X, T = inputs(15, 64, 2, 64, 16, 100)
+    packed = net.pack(W.to(gpu))
+    Xd = torch.empty(100 * 64 + 8, dtype=torch.bfloat16, device=gpu)[1:1 + 100 * 64].view(100, 64)
+    with pytest.raises(ffmlp.FFMLPError) as e:
+        net.forward(packed, Xd)
+    assert e.value.code == ffmlp.MLP_ERR_INVALID_ARG
