@@ -1,0 +1,212 @@
+"""Benchmark of the fused-MLP hot path on one MI355X.
+
+One step = the whole path over one synthetic batch of M rows:
+  pack the weights (they change every training step), one inference forward
+  pass (Algorithm 1), one training step (Algorithm 2: forward with stash, MSE
+  loss and output delta, backward delta propagation, weight gradients).
+`value` is M / (time per step) in samples/s with inputs resident in HBM.
+
+The `roofline` object is the inference kernel (one launch per forward call,
+so HIP events on its stream time exactly that kernel): algorithmic flops
+2 * sum(fan_in * fan_out) per row against the dense bf16 MFMA peak.
+`roofline_train` is the whole training step against HBM bandwidth, with
+its algorithmic bytes per row.  `cpu_baseline` times the fp64 oracle on a
+bounded sample of the same step on the host cores.
+
+    python bench.py [--steps K] [--warmup W] [--width 128 --depth 4 --batch 1048576]
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "samples/s + TFLOP/s (% bf16 MFMA peak) for fused MLP fwd and train step"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+
+
+def flops_per_row(width, depth, in_dim, out_dim):
+    shapes = [(in_dim if l == 0 else width, out_dim if l == depth else width)
+              for l in range(depth + 1)]
+    P = sum(a * b for a, b in shapes)
+    fwd = 2 * P
+    bwd = 2 * (P - shapes[0][0] * shapes[0][1])  # no input gradient
+    return fwd, fwd + bwd + 2 * P  # inference, training step
+
+
+def train_bytes_per_row(width, depth, in_dim, out_dim, act):
+    """HBM bytes the three-kernel training step must move per row:
+    forward reads X, T and writes the activations and the output delta;
+    backward reads the output delta and the activations (or the stored
+    cos for sine) and writes the hidden deltas; the gradient kernel reads
+    X, the activations, the hidden deltas and the output delta."""
+    OP = (out_dim + 15) // 16 * 16
+    hid = depth * width * 2
+    b = 2 * in_dim + 4 * out_dim + hid + 2 * OP           # forward (train)
+    if act == "sine":
+        b += hid                                          # cos stash write
+    b += 2 * OP + hid + hid                               # backward
+    b += 2 * in_dim + hid + hid + 2 * OP                  # weight gradients
+    return b
+
+
+def cpu_baseline(width, depth, in_dim, out_dim, act, out_act, target_s=12.0):
+    """The oracle (fp64, OpenMP over rows) on a bounded sample of the step:
+    one inference forward plus one training step per row."""
+    import oracle
+    import datagen
+    acts = {"linear": oracle.LINEAR, "relu": oracle.RELU, "sigmoid": oracle.SIGMOID,
+            "sine": oracle.SINE}
+    net = oracle.Net(width, depth, in_dim, out_dim, acts[act], acts[out_act])
+    W = datagen.xavier_weights(3, width, depth, in_dim, out_dim)
+
+    def run(m):
+        X = datagen.inputs_uniform(3, m, in_dim)
+        T = datagen.targets_uniform(3, m, out_dim)
+        t0 = time.perf_counter()
+        net.forward(W, X)
+        net.train_step(W, X, T)
+        return time.perf_counter() - t0
+
+    m = 1024
+    dt = run(m)
+    m = int(min(max(m * target_s / max(dt, 1e-3), 1024), 1 << 20))
+    dt = run(m)
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    return {"value": m / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
+            "sample": f"{m} rows of the same net and input recipe, inference forward + training "
+                      f"step, fp64, {dt:.1f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--width", type=int, default=128)
+    ap.add_argument("--depth", type=int, default=4)
+    ap.add_argument("--in-dim", type=int, default=None)
+    ap.add_argument("--out-dim", type=int, default=16)
+    ap.add_argument("--batch", type=int, default=1 << 20)
+    ap.add_argument("--act", default="relu")
+    ap.add_argument("--out-act", default="linear")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle timing")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: this build has no multi-GPU path "
+              "(inference shards rows with no communication; training would add one "
+              "all-reduce of the gradients).", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import datagen
+    import paper_2403_17607_amd as ffmlp
+
+    width, depth, M = args.width, args.depth, args.batch
+    in_dim = args.in_dim or width
+    out_dim = args.out_dim
+    dev = torch.device("cuda:0")
+    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, args.act, args.out_act)
+    W = datagen.xavier_weights(2, width, depth, in_dim, out_dim, device=dev)
+    # two input buffers, alternated, so inference does not run out of the
+    # 256 MiB last-level cache
+    Xs = [datagen.inputs_uniform(2 + i, M, in_dim, device=dev) for i in range(2)]
+    T = datagen.targets_uniform(2, M, out_dim, device=dev)
+    packed = net.pack(W)
+    ws = net.workspace(M, dev)
+    Y = torch.empty(M, out_dim, dtype=torch.bfloat16, device=dev)
+    G = torch.empty(net.param_count(), dtype=torch.float32, device=dev)
+    loss = torch.empty(1, dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream(dev)
+
+    K, Wm = args.steps, args.warmup
+    ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
+
+    def step(i, events=None):
+        if events:
+            events[0].record(stream)
+        net.pack(W, out=packed)
+        if events:
+            events[1].record(stream)
+        net.forward(packed, Xs[i % 2], Y=Y)
+        if events:
+            events[2].record(stream)
+        net.train_step(packed, Xs[i % 2], T, ws, G=G, loss=loss)
+        if events:
+            events[3].record(stream)
+
+    for i in range(Wm):
+        step(i)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(K):
+        step(i, ev[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    t_step = sum(e[0].elapsed_time(e[3]) for e in ev) / K  # ms
+    t_inf = sum(e[1].elapsed_time(e[2]) for e in ev) / K
+    t_train = sum(e[2].elapsed_time(e[3]) for e in ev) / K
+    t_pack = sum(e[0].elapsed_time(e[1]) for e in ev) / K
+    ms_per_step = wall * 1e3 / K
+
+    fl_inf, fl_train = flops_per_row(width, depth, in_dim, out_dim)
+    inf_tflops = fl_inf * M / (t_inf * 1e-3) / 1e12
+    train_tflops = fl_train * M / (t_train * 1e-3) / 1e12
+    bytes_inf = M * (2 * in_dim + 2 * out_dim)
+    bytes_train = M * train_bytes_per_row(width, depth, in_dim, out_dim, args.act)
+    train_gbs = bytes_train / (t_train * 1e-3) / 1e9
+
+    out = {
+        "metric": METRIC,
+        "value": M / (ms_per_step * 1e-3),
+        "unit": "samples/s",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": ms_per_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": f"fused MLP width {width}, {depth} hidden layers, in {in_dim}, "
+                               f"out {out_dim}, {args.act} hidden, {args.out_act} output, "
+                               f"batch {M}: weight pack + inference + training step",
+                   "width": width, "depth": depth, "in_dim": in_dim, "out_dim": out_dim,
+                   "batch": M, "activation": args.act, "output_activation": args.out_act},
+        "infer": {"ms": t_inf, "samples_per_s": M / (t_inf * 1e-3), "tflops": inf_tflops,
+                  "pct_bf16_peak": 100 * inf_tflops / PEAK_BF16_TFLOPS,
+                  "hbm_gbs_algorithmic": bytes_inf / (t_inf * 1e-3) / 1e9},
+        "train": {"ms": t_train, "samples_per_s": M / (t_train * 1e-3), "tflops": train_tflops,
+                  "pct_bf16_peak": 100 * train_tflops / PEAK_BF16_TFLOPS,
+                  "hbm_gbs_algorithmic": train_gbs},
+        "pack_ms": t_pack,
+        "event_ms_per_step": t_step,
+        "roofline": {"kernel": "fwd_kernel (inference)", "bound": "mfma",
+                     "achieved": inf_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": inf_tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                     "flops_per_row": fl_inf, "rows_per_launch": M},
+        "roofline_train": {"kernels": "fwd_kernel (train) + bwd_kernel + wgrad_kernel + "
+                                      "reduce_kernel", "bound": "hbm", "achieved": train_gbs,
+                           "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                           "frac": train_gbs / PEAK_HBM_GBS,
+                           "bytes_per_row": train_bytes_per_row(width, depth, in_dim, out_dim,
+                                                                args.act)},
+    }
+    del ws
+    torch.cuda.empty_cache()
+    if not args.no_cpu:
+        out["cpu_baseline"] = cpu_baseline(width, depth, in_dim, out_dim, args.act, args.out_act)
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,13 +1,21 @@
 """Shared pieces of the parity tests: seeded inputs (from datagen), the
 oracle's view of a net, and the two error measures with their bounds.
 
-Bounds (per output and per weight-gradient matrix):
-  outputs    max_i |Y_i - Yref_i| / max(|Yref_i|, rms(Yref)) <= 2e-2
-  gradients  ||G_l - Gref_l||_F / ||Gref_l||_F <= 1e-2
-The GPU rounds to bf16 at the same points as the oracle; what differs is
-the fp32 (GPU) versus fp64 (oracle) accumulation, which can move a value
-across a bf16 rounding boundary (one bf16 ulp = 2^-8 relative) and those
-flips propagate through later layers.
+Bounds (per output and per weight-gradient matrix), for a net with L
+weight matrices:
+  outputs    max_i |Y_i - Yref_i| / max(|Yref_i|, rms(Yref)) <= 2e-2 s(L)
+             ||Y - Yref||_F / ||Yref||_F <= 2e-3
+             99.9th percentile of the per-element error above <= 2e-2
+  gradients  ||G_l - Gref_l||_F / ||Gref_l||_F <= 1e-2 s(L)
+with s(L) = max(1, L / 5).  The GPU rounds to bf16 at the same points as the
+oracle; what differs is the fp32 (GPU) versus fp64 (oracle) accumulation,
+which can move a value across a bf16 rounding boundary (one bf16 ulp =
+2^-8 relative), and every such flip propagates through the later layers.
+The number of rounding stages grows with L, so the worst-element bounds
+(2e-2 and 1e-2, stated for nets of up to 5 matrices) scale with L / 5; a
+CPU model with fp32 sums and the same rounding points departs from the
+oracle by as much (3.5e-2 on outputs, 1.5e-2 on gradients at L = 17).  The
+aggregate bounds do not scale.
 """
 from __future__ import annotations
 
@@ -20,6 +28,12 @@ import oracle
 OUT_TOL = 2e-2
 GRAD_TOL = 1e-2
 LOSS_TOL = 1e-3
+OUT_FRO_TOL = 2e-3
+OUT_P999_TOL = 2e-2
+
+
+def depth_scale(n_mats: int) -> float:
+    return max(1.0, n_mats / 5.0)
 
 ACT = {"linear": 0, "relu": 1, "sigmoid": 2, "sine": 3}
 
@@ -40,13 +54,38 @@ def f64(t):
     return t.detach().to("cpu").to(torch.float64).numpy()
 
 
-def out_err(Y, Yref) -> float:
+def _elem_err(Y, Yref):
     Y, Yref = np.asarray(Y, np.float64), np.asarray(Yref, np.float64)
-    if Yref.size == 0:
-        return 0.0
     rms = float(np.sqrt(np.mean(Yref ** 2)))
     denom = np.maximum(np.abs(Yref), rms if rms > 0 else 1.0)
-    return float(np.max(np.abs(Y - Yref) / denom))
+    return np.abs(Y - Yref) / denom
+
+
+def out_err(Y, Yref) -> float:
+    if np.asarray(Yref).size == 0:
+        return 0.0
+    return float(np.max(_elem_err(Y, Yref)))
+
+
+def check_outputs(Y, Yref, n_mats: int) -> dict:
+    """Assert the three output bounds; returns the measured errors."""
+    Y, Yref = np.asarray(Y, np.float64), np.asarray(Yref, np.float64)
+    if Yref.size == 0:
+        return {}
+    e = _elem_err(Y, Yref)
+    nref = np.linalg.norm(Yref)
+    fro = float(np.linalg.norm(Y - Yref) / nref) if nref > 0 else float(np.linalg.norm(Y))
+    res = {"max": float(e.max()), "p999": float(np.quantile(e, 0.999)), "fro": fro}
+    assert res["max"] <= OUT_TOL * depth_scale(n_mats), res
+    assert res["p999"] <= OUT_P999_TOL, res
+    assert res["fro"] <= OUT_FRO_TOL, res
+    return res
+
+
+def check_grads(G, Gref, net) -> list[float]:
+    errs = grad_errs(G, Gref, net)
+    assert max(errs) <= GRAD_TOL * depth_scale(net.L), errs
+    return errs
 
 
 def grad_errs(G, Gref, net) -> list[float]:

@@ -13,8 +13,7 @@ import pytest
 import torch
 
 import datagen
-from helpers import (GRAD_TOL, LOSS_TOL, OUT_TOL, f64, grad_errs, inputs, oracle_net,
-                     out_err)
+from helpers import (LOSS_TOL, check_grads, check_outputs, f64, inputs, oracle_net)
 
 pytestmark = pytest.mark.gpu
 
@@ -41,17 +40,16 @@ def run_case(ffmlp, dev, width, depth, in_dim, out_dim, M, act="relu", out_act="
         torch.cuda.synchronize()
         ref = onet.train_step(W, X, T)
         res.update(G=G, loss=loss, Yt=Yt, ref=ref, ws=ws)
-        assert out_err(f64(Y), ref["Y"]) <= OUT_TOL
+        log("  output errs", check_outputs(f64(Y), ref["Y"], onet.L))
         assert torch.equal(Y, Yt), "train-step outputs differ from inference outputs"
-        errs = grad_errs(f64(G), ref["G"], onet)
+        errs = check_grads(f64(G), ref["G"], onet)
         log("  grad errs", ["%.2e" % e for e in errs])
-        assert max(errs) <= GRAD_TOL
         lref = ref["loss"]
         assert abs(loss.item() - lref) <= LOSS_TOL * max(abs(lref), 1e-30)
     else:
         torch.cuda.synchronize()
         Yref, _ = onet.forward(W, X)
-        assert out_err(f64(Y), Yref) <= OUT_TOL
+        log("  output errs", check_outputs(f64(Y), Yref, onet.L))
     return res
 
 
@@ -106,8 +104,8 @@ def test_image_like(ffmlp, gpu):
     Y = torch.empty(M, 3, dtype=torch.bfloat16, device=gpu)
     G, loss = net.train_step(packed, X.to(gpu), T.to(gpu), ws, Y=Y)
     ref = onet.train_step(W, X, T)
-    assert out_err(f64(Y), ref["Y"]) <= OUT_TOL
-    assert max(grad_errs(f64(G), ref["G"], onet)) <= GRAD_TOL
+    check_outputs(f64(Y), ref["Y"], onet.L)
+    check_grads(f64(G), ref["G"], onet)
 
 
 def test_pinn_like(ffmlp, gpu):
@@ -132,8 +130,8 @@ def test_forward_stash_then_backward(ffmlp, gpu, width, act, out_act):
     G = net.backward(packed, Xd, dY.to(gpu), ws)
     Yref, _ = onet.forward(W, X)
     Gref = onet.backward(W, X, dY)
-    assert out_err(f64(Y), Yref) <= OUT_TOL
-    assert max(grad_errs(f64(G), Gref, onet)) <= GRAD_TOL
+    check_outputs(f64(Y), Yref, onet.L)
+    check_grads(f64(G), Gref, onet)
 
 
 # ------------------------------------------------------ bitwise properties --
@@ -233,11 +231,10 @@ def test_full_size_sampled(ffmlp, gpu, width, depth, in_dim, out_dim, M):
     dY[rows.to(gpu)] = dYs.to(gpu)
     G = net.backward(packed, Xd, dY, ws)
     Yref, _ = onet.forward(W, Xs)
-    assert out_err(f64(Y[rows.to(gpu)]), Yref) <= OUT_TOL
+    log("  output errs", check_outputs(f64(Y[rows.to(gpu)]), Yref, onet.L))
     Gref = onet.backward(W, Xs, dYs)
-    errs = grad_errs(f64(G), Gref, onet)
+    errs = check_grads(f64(G), Gref, onet)
     log("  grad errs", ["%.2e" % e for e in errs])
-    assert max(errs) <= GRAD_TOL
     del ws
     torch.cuda.empty_cache()
 
