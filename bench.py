@@ -75,10 +75,10 @@ def cpu_baseline(width, depth, in_dim, out_dim, act, out_act, target_s=12.0):
         net.train_step(W, X, T)
         return time.perf_counter() - t0
 
-    m = 1024
-    dt = run(m)
-    m = int(min(max(m * target_s / max(dt, 1e-3), 1024), 1 << 20))
-    dt = run(m)
+    m, dt = 4096, run(4096)
+    while dt < 0.8 * target_s and m < (1 << 22):
+        m = int(min(max(m * target_s / max(dt, 1e-3), 2 * m), 1 << 22))
+        dt = run(m)
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
     return {"value": m / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
             "sample": f"{m} rows of the same net and input recipe, inference forward + training "

@@ -76,7 +76,7 @@ PackGeom pack_geom(const mlp* h) {
 // Workspace layout for a batch of M rows (byte offsets, 256-byte aligned).
 struct WsLayout {
   int64_t M16;
-  size_t stashA, stashS, deltaH, deltaOut, cOut, partial, lossPart, total;
+  size_t stashA, stashS, deltaH, deltaOut, cOut, partial, mid, lossPart, total;
   int P, chunks_per_block;
 };
 
@@ -104,6 +104,7 @@ WsLayout ws_layout(const mlp* h, int64_t M) {
   int64_t params = 0;
   for (int l = 0; l < L; ++l) params += (int64_t)fan_in_of(h, l) * fan_out_of(h, l);
   w.partial = o; o = round_up(o + (size_t)P * params * 4, 256);
+  w.mid = o; o = round_up(o + (size_t)kReduceSlices * params * 4, 256);
   w.lossPart = o; o = round_up(o + (size_t)kMaxLossParts * 4, 256);
   w.total = o;
   return w;
@@ -186,6 +187,7 @@ int run_wgrad_reduce(const mlp* h, const uint16_t* X, const WsLayout& w, uint8_t
   }
   ReduceArgs r{};
   r.partial = reinterpret_cast<const float*>(ws + w.partial);
+  r.mid = reinterpret_cast<float*>(ws + w.mid);
   r.G = G;
   r.params = params;
   r.P = M > 0 ? w.P : 0;
@@ -287,41 +289,16 @@ int mlp_pack_weights(const mlp_t* h, const uint16_t* W, void* packed, void* stre
   if (!W || !packed) return fail(MLP_ERR_INVALID_ARG, "null weight or packed pointer");
   if (!aligned(W, 2) || !aligned(packed, 16))
     return fail(MLP_ERR_INVALID_ARG, "W must be 2-byte and packed 16-byte aligned");
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  const int L = n_mats(h);
-  uint16_t* dst = static_cast<uint16_t*>(packed);
-  int64_t woff = 0;
-  for (int l = 0; l < L; ++l) {
-    PackArgs a{};
-    a.W = W + woff;
-    a.fan_in = fan_in_of(h, l);
-    a.fan_out = fan_out_of(h, l);
-    a.strips = strips(a.fan_out);
-    a.kblocks = kblocks(a.fan_in);
-    a.dir = 0;
-    a.first = l == 0;
-    a.dst = dst;
-    hipError_t e = launch_pack(a, s);
-    if (e != hipSuccess) return hip_fail(e, "pack kernel launch");
-    dst += (size_t)a.strips * a.kblocks * 512;
-    woff += (int64_t)a.fan_in * a.fan_out;
-  }
-  woff = (int64_t)fan_in_of(h, 0) * fan_out_of(h, 0);
-  for (int l = 1; l < L; ++l) {
-    PackArgs a{};
-    a.W = W + woff;
-    a.fan_in = fan_in_of(h, l);
-    a.fan_out = fan_out_of(h, l);
-    a.strips = strips(a.fan_in);
-    a.kblocks = kblocks(a.fan_out);
-    a.dir = 1;
-    a.first = 0;
-    a.dst = dst;
-    hipError_t e = launch_pack(a, s);
-    if (e != hipSuccess) return hip_fail(e, "pack kernel launch");
-    dst += (size_t)a.strips * a.kblocks * 512;
-    woff += (int64_t)a.fan_in * a.fan_out;
-  }
+  PackArgs a{};
+  a.W = W;
+  a.dst = static_cast<uint16_t*>(packed);
+  a.width = h->width;
+  a.in_dim = h->in_dim;
+  a.out_dim = h->out_dim;
+  a.L = n_mats(h);
+  a.total = (int64_t)(mlp_packed_bytes(h) / 2);
+  hipError_t e = launch_pack(a, static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_fail(e, "pack kernel launch");
   return MLP_OK;
 }
 

@@ -21,7 +21,8 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
   constexpr int NT = TileCfg<W>::NT, NW = TileCfg<W>::NW, NTH = NW * 64;
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
   extern __shared__ u32x4 smem[];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int li = lane & 15, lg = lane >> 4;
   const int L = a.L, out_dim = a.out_dim, out_act = a.out_act;
   const int64_t M = a.M;

@@ -69,9 +69,11 @@ inline int tile_rows(int width) {
 // 16x16 output tiles; GK x GJ blocks cover G; KS waves split every chunk of
 // the batch; each wave runs KSW 32-row contraction steps per chunk.
 template <int W> struct WgCfg;
-template <> struct WgCfg<16> { static constexpr int TBK = 1, TBJ = 1, GK = 1, GJ = 1, KS = 4, KSW = 1; };
-template <> struct WgCfg<32> { static constexpr int TBK = 2, TBJ = 2, GK = 1, GJ = 1, KS = 4, KSW = 1; };
-template <> struct WgCfg<64> { static constexpr int TBK = 4, TBJ = 4, GK = 1, GJ = 1, KS = 4, KSW = 1; };
+// The chunk is CH = 32 KS KSW rows, so CH * W / 8 = 1024 16-byte units per
+// tensor at every width (four per thread).
+template <> struct WgCfg<16> { static constexpr int TBK = 1, TBJ = 1, GK = 1, GJ = 1, KS = 4, KSW = 4; };
+template <> struct WgCfg<32> { static constexpr int TBK = 2, TBJ = 2, GK = 1, GJ = 1, KS = 4, KSW = 2; };
+template <> struct WgCfg<64> { static constexpr int TBK = 2, TBJ = 2, GK = 2, GJ = 2, KS = 1, KSW = 4; };
 template <> struct WgCfg<128> { static constexpr int TBK = 4, TBJ = 4, GK = 2, GJ = 2, KS = 1, KSW = 2; };
 template <int W> constexpr int wg_chunk() { return 32 * WgCfg<W>::KS * WgCfg<W>::KSW; }
 inline int wgrad_chunk(int width) {
@@ -128,8 +130,13 @@ struct WgradArgs {
   int P, chunks_per_block;
 };
 
+// Fixed-order sum of the P weight-gradient partials in two passes: pass 1
+// adds slice y (partials [y P / S, (y+1) P / S)) into mid[y]; pass 2 adds
+// the S slices in order into G and sums the loss partials.
+constexpr int kReduceSlices = 16;
 struct ReduceArgs {
-  const float* partial;
+  const float* partial;  // [P][params]
+  float* mid;            // [kReduceSlices][params]
   float* G;
   int64_t params;
   int P;
@@ -140,11 +147,10 @@ struct ReduceArgs {
 };
 
 struct PackArgs {
-  const uint16_t* W;  // this layer's weights, [fan_in][fan_out]
-  uint16_t* dst;      // this layer's packed fragments
-  int fan_in, fan_out, strips, kblocks;
-  int dir;            // 0 forward, 1 backward
-  int first;          // forward layer 0: input order instead of chain order
+  const uint16_t* W;  // all weights, concatenated [fan_in][fan_out] matrices
+  uint16_t* dst;      // packed buffer: forward layers, then backward layers
+  int width, in_dim, out_dim, L;
+  int64_t total;      // bf16 elements of the packed buffer
 };
 
 // Host-side launchers (one per translation unit).  They return a HIP error.

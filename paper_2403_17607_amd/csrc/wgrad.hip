@@ -5,14 +5,16 @@
 // The paper computes these products outside its fused kernel with library
 // GEMMs; here one kernel covers every layer (grid.y = layer) as a split-K
 // MFMA contraction: workgroup p of a layer sums its own contiguous range of
-// batch rows into an fp32 partial G, and a second kernel adds the P partials
+// batch rows into an fp32 partial G, and two small passes add the P partials
 // in a fixed order, so G is bitwise reproducible.
 //
 // A matrix-core operand for a contraction over the batch needs eight batch
 // rows of one feature per lane, while the stash holds each batch row's
 // features together.  Each chunk of rows is therefore transposed on its way
 // into LDS (feature-major, batch contiguous), and every operand fragment is
-// then a single 16-byte LDS read.
+// then a single 16-byte LDS read.  The next chunk's global loads are issued
+// into registers before the current chunk's MFMAs, so HBM traffic overlaps
+// the contraction.
 #include "device.h"
 
 namespace ffmlp {
@@ -22,16 +24,23 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   using C = WgCfg<W>;
   constexpr int TBK = C::TBK, TBJ = C::TBJ, GJ = C::GJ, KS = C::KS, KSW = C::KSW;
   constexpr int CH = wg_chunk<W>();
-  constexpr int LDT = CH + 8;  // LDS row stride (elements) of the transposed tiles
+  constexpr int LDT = CH + 8;      // LDS row stride (bf16) of the transposed tiles
+  constexpr int LDW = LDT / 2;     // the same in 32-bit words
+  constexpr int UPT = CH * W / 8 / 256;  // 16-byte units per thread per tensor
+  static_assert(UPT >= 2 && UPT % 2 == 0, "chunk geometry");
   extern __shared__ u32x4 smem_v[];
   uint16_t* AT = reinterpret_cast<uint16_t*>(smem_v);
   uint16_t* DT = AT + W * LDT;
+  uint32_t* AT32 = reinterpret_cast<uint32_t*>(AT);
+  uint32_t* DT32 = reinterpret_cast<uint32_t*>(DT);
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int li = lane & 15, lg = lane >> 4;
   const int l = blockIdx.y, p = blockIdx.x, L = a.L;
   const int64_t M = a.M;
-  const int fan_in = (l == 0) ? a.in_dim : W;
+  const int in_dim = a.in_dim;
+  const int fan_in = (l == 0) ? in_dim : W;
   const int fan_out = (l == L - 1) ? a.out_dim : W;
   const int OP = ((a.out_dim + 15) >> 4) * 16;
   const int KT = (fan_in + 15) >> 4, JT = (fan_out + 15) >> 4;
@@ -40,8 +49,97 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
 
   const uint16_t* dsrc = (l == L - 1) ? a.deltaOut : a.deltaH + (size_t)l * a.M16 * W;
   const int dF = (l == L - 1) ? OP : W;
-  const uint16_t* asrc = (l == 0) ? nullptr : a.stashA + (size_t)(l - 1) * a.M16 * W;
-  const bool xvec = (a.in_dim & 7) == 0;
+  const uint16_t* asrc = (l == 0) ? a.X : a.stashA + (size_t)(l - 1) * a.M16 * W;
+  const bool xvec = (in_dim & 7) == 0;
+  const int nf8 = (in_dim + 7) >> 3;  // 8-feature groups of an X row
+
+  u32x4 ra[UPT], rd[UPT];
+
+  // ---- global -> registers ----
+  // The loads are unconditional (an out-of-range unit reads the tensor's
+  // first 16 bytes instead) so that all of a chunk's loads are in flight
+  // together; rows past M are zeroed when the registers go to LDS.
+  //
+  // Tile-image tensor with F features: unit v covers rows 16 tl + 2 ip,
+  // +1 and features 16 s + 4 g + 0..3.  Consecutive lanes take consecutive
+  // ip then tl, so a wave's transposed LDS writes hit distinct banks while
+  // every 8 lanes still read one contiguous 128-byte line.
+  struct TileUnit {
+    int tl, s, g, ip;
+  };
+  auto tile_unit = [&](int v, int S) {
+    const int ip = v & 7, tla = (v >> 3) & 3, rest2 = v >> 5;
+    const int g = rest2 & 3, rest3 = rest2 >> 2;
+    return TileUnit{(rest3 / S) * 4 + tla, rest3 % S, g, ip};
+  };
+  auto addr_tile = [&](const uint16_t* (&pa)[UPT], const uint16_t* src, int F, int64_t c0) {
+    const int S = F >> 4;
+    const int U = CH * F / 8;
+#pragma unroll
+    for (int k = 0; k < UPT; ++k) {
+      const int v = k * 256 + tid;
+      const TileUnit t = tile_unit(v, S);
+      const bool ok = v < U && c0 + 16 * t.tl < M;
+      pa[k] = src + (ok ? (size_t)c0 * F + ((size_t)((t.tl * S + t.s) * 4 + t.g) * 8 + t.ip) * 8 : 0);
+    }
+  };
+  // X (row-major [M][in_dim], in_dim a multiple of 8): unit pair q covers
+  // rows 2 j, 2 j + 1 and features 8 f8 .. + 7; consecutive lanes take
+  // consecutive j.
+  auto addr_x = [&](const uint16_t* (&pa)[UPT], int64_t c0) {
+    const int npairs = (CH / 2) * nf8;
+#pragma unroll
+    for (int k = 0; k < UPT / 2; ++k) {
+      const int q = k * 256 + tid;
+      const int j = q % (CH / 2), f0 = (q / (CH / 2)) * 8;
+      const int64_t row = c0 + 2 * j;
+      const bool ok0 = q < npairs && row < M, ok1 = q < npairs && row + 1 < M;
+      pa[2 * k] = a.X + (ok0 ? row * in_dim + f0 : 0);
+      pa[2 * k + 1] = a.X + (ok1 ? (row + 1) * in_dim + f0 : 0);
+    }
+  };
+  // ---- registers -> LDS, transposed to [feature][batch row] ----
+  auto store_tile = [&](const u32x4 (&r)[UPT], uint32_t* T32, int F, int64_t c0) {
+    const int S = F >> 4;
+    const int U = CH * F / 8;
+#pragma unroll
+    for (int k = 0; k < UPT; ++k) {
+      const int v = k * 256 + tid;
+      if (v < U) {
+        const TileUnit t = tile_unit(v, S);
+        const int64_t row = c0 + 16 * t.tl + 2 * t.ip;
+        u32x4 x = r[k];
+        if (row >= M) { x.x = 0u; x.y = 0u; }
+        if (row + 1 >= M) { x.z = 0u; x.w = 0u; }
+        uint32_t* d = T32 + (16 * t.s + 4 * t.g) * LDW + 8 * t.tl + t.ip;
+        d[0 * LDW] = (x.x & 0xffffu) | (x.z << 16);
+        d[1 * LDW] = (x.x >> 16) | (x.z & 0xffff0000u);
+        d[2 * LDW] = (x.y & 0xffffu) | (x.w << 16);
+        d[3 * LDW] = (x.y >> 16) | (x.w & 0xffff0000u);
+      }
+    }
+  };
+  auto store_x = [&](const u32x4 (&r)[UPT], int64_t c0) {
+    const int npairs = (CH / 2) * nf8;
+#pragma unroll
+    for (int k = 0; k < UPT / 2; ++k) {
+      const int q = k * 256 + tid;
+      if (q < npairs) {
+        const int j = q % (CH / 2), f0 = (q / (CH / 2)) * 8;
+        const int64_t row = c0 + 2 * j;
+        u32x4 x0 = r[2 * k], x1 = r[2 * k + 1];
+        if (row >= M) x0 = u32x4{0u, 0u, 0u, 0u};
+        if (row + 1 >= M) x1 = u32x4{0u, 0u, 0u, 0u};
+        const uint32_t w0[4] = {x0.x, x0.y, x0.z, x0.w}, w1[4] = {x1.x, x1.y, x1.z, x1.w};
+        uint32_t* d = AT32 + f0 * LDW + j;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          d[(2 * e) * LDW] = (w0[e] & 0xffffu) | (w1[e] << 16);
+          d[(2 * e + 1) * LDW] = (w0[e] >> 16) | (w1[e] & 0xffff0000u);
+        }
+      }
+    }
+  };
 
   f32x4 acc[TBK][TBJ];
 #pragma unroll
@@ -54,68 +152,42 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   int64_t c_end = c_begin + a.chunks_per_block;
   if (c_end > nch) c_end = nch;
 
+  // Other input widths: X goes straight from global memory into LDS,
+  // element by element, when the chunk is stored (no register staging).
+  auto copy_x_scalar = [&](int64_t c0) {
+    for (int u = tid; u < CH * in_dim; u += 256) {
+      const int ml = u / in_dim, f = u - ml * in_dim;
+      const int64_t row = c0 + ml;
+      AT[(size_t)f * LDT + ml] = row < M ? a.X[row * in_dim + f] : (uint16_t)0;
+    }
+  };
+  // Addresses first (uniform branches), then one unconditional load per
+  // unit, so the loads of a chunk are all in flight together.
+  auto load_chunk = [&](int64_t c) {
+    const uint16_t* pa[UPT];
+    const uint16_t* pd[UPT];
+    if (l != 0) addr_tile(pa, asrc, W, c * CH);
+    else if (xvec) addr_x(pa, c * CH);
+    else {
+#pragma unroll
+      for (int k = 0; k < UPT; ++k) pa[k] = a.X;
+    }
+    addr_tile(pd, dsrc, dF, c * CH);
+#pragma unroll
+    for (int k = 0; k < UPT; ++k) ra[k] = *reinterpret_cast<const u32x4*>(pa[k]);
+#pragma unroll
+    for (int k = 0; k < UPT; ++k) rd[k] = *reinterpret_cast<const u32x4*>(pd[k]);
+  };
+
+  if (c_begin < c_end) load_chunk(c_begin);
   for (int64_t c = c_begin; c < c_end; ++c) {
-    const int64_t c0 = c * CH;
+    __syncthreads();  // every wave is done reading the previous chunk
+    if (l != 0) store_tile(ra, AT32, W, c * CH);
+    else if (xvec) store_x(ra, c * CH);
+    else copy_x_scalar(c * CH);
+    store_tile(rd, DT32, dF, c * CH);
     __syncthreads();
-    // ---- A chunk -> AT[f][m] ----
-    if (l == 0) {
-      const int in_dim = a.in_dim;
-      if (xvec) {
-        const int units = CH * in_dim / 8;
-        for (int u = tid; u < units; u += 256) {
-          const int e = u * 8;
-          const int ml = e / in_dim, f = e - ml * in_dim;
-          const int64_t row = c0 + ml;
-          u32x4 v = {0u, 0u, 0u, 0u};
-          if (row < M) v = *reinterpret_cast<const u32x4*>(a.X + row * in_dim + f);
-          uint16_t* t = AT + (size_t)f * LDT + ml;
-          t[0 * LDT] = (uint16_t)(v.x & 0xffff);
-          t[1 * LDT] = (uint16_t)(v.x >> 16);
-          t[2 * LDT] = (uint16_t)(v.y & 0xffff);
-          t[3 * LDT] = (uint16_t)(v.y >> 16);
-          t[4 * LDT] = (uint16_t)(v.z & 0xffff);
-          t[5 * LDT] = (uint16_t)(v.z >> 16);
-          t[6 * LDT] = (uint16_t)(v.w & 0xffff);
-          t[7 * LDT] = (uint16_t)(v.w >> 16);
-        }
-      } else {
-        const int units = CH * in_dim;
-        for (int u = tid; u < units; u += 256) {
-          const int ml = u / in_dim, f = u - ml * in_dim;
-          const int64_t row = c0 + ml;
-          AT[(size_t)f * LDT + ml] = (row < M) ? a.X[row * in_dim + f] : (uint16_t)0;
-        }
-      }
-    }
-    // Tile-image sources: 8 elements = rows i, i+1 (i even) x features
-    // 16 s + 4 g + 0..3 of one 16-row block.
-    for (int pass = (l == 0) ? 1 : 0; pass < 2; ++pass) {
-      const uint16_t* src = pass == 0 ? asrc : dsrc;
-      const int F = pass == 0 ? W : dF;
-      uint16_t* T = pass == 0 ? AT : DT;
-      const int units = CH * F / 8;
-      for (int u = tid; u < units; u += 256) {
-        const int e = u * 8;
-        const int tl = e / (16 * F);
-        const int rem = e - tl * 16 * F;
-        const int s = rem >> 8, w = rem & 255;
-        const int ln = w >> 2, g = ln >> 4, i = ln & 15;
-        const int64_t row = c0 + 16 * tl + i;
-        u32x4 v = {0u, 0u, 0u, 0u};
-        if (c0 + 16 * tl < M) v = *reinterpret_cast<const u32x4*>(src + (size_t)c0 * F + e);
-        if (row >= M) { v.x = 0u; v.y = 0u; }
-        if (row + 1 >= M) { v.z = 0u; v.w = 0u; }
-        const int f = 16 * s + 4 * g;
-        uint32_t* t = reinterpret_cast<uint32_t*>(T + (size_t)f * LDT + 16 * tl + i);
-        constexpr int LDW = LDT / 2;
-        t[0 * LDW] = (v.x & 0xffffu) | (v.z << 16);
-        t[1 * LDW] = (v.x >> 16) | (v.z & 0xffff0000u);
-        t[2 * LDW] = (v.y & 0xffffu) | (v.w << 16);
-        t[3 * LDW] = (v.y >> 16) | (v.w & 0xffff0000u);
-      }
-    }
-    __syncthreads();
-    // ---- contraction over the chunk's batch rows ----
+    if (c + 1 < c_end) load_chunk(c + 1);
 #pragma unroll
     for (int q = 0; q < KSW; ++q) {
       const int koff = (wks * KSW + q) * 32 + lg * 8;
@@ -155,17 +227,19 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
     __syncthreads();
     if (wks != 0) return;
 #pragma unroll
-    for (int k = 1; k < KS; ++k)
+    for (int k = 1; k < KS; ++k) {
 #pragma unroll
       for (int tk = 0; tk < TBK; ++tk)
 #pragma unroll
         for (int tj = 0; tj < TBJ; ++tj)
           acc[tk][tj] += red[(((blk * (KS - 1) + k - 1) * TBK + tk) * TBJ + tj) * 64 + lane];
+      __builtin_amdgcn_sched_barrier(0);  // one partial at a time: bounds the registers
+    }
   }
 
   // Partial G of this workgroup, in the weights' own layout.
   int64_t off = 0;
-  if (l >= 1) off = (int64_t)a.in_dim * W + (int64_t)(l - 1) * W * W;
+  if (l >= 1) off = (int64_t)in_dim * W + (int64_t)(l - 1) * W * W;
   float* dst = a.partial + (int64_t)p * a.params + off;
 #pragma unroll
   for (int tk = 0; tk < TBK; ++tk) {
@@ -183,40 +257,84 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   }
 }
 
-__global__ __launch_bounds__(256) void reduce_kernel(const ReduceArgs a) {
+// Pass 1: mid[y][e] = sum of partial[p][e] over slice y of p, in order.
+__global__ __launch_bounds__(256) void reduce1_kernel(const ReduceArgs a) {
+  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int y = blockIdx.y;
+  if (e >= a.params) return;
+  const int p0 = (int)((int64_t)a.P * y / kReduceSlices);
+  const int p1 = (int)((int64_t)a.P * (y + 1) / kReduceSlices);
+  float s = 0.f;
+  for (int p = p0; p < p1; ++p) s += a.partial[(int64_t)p * a.params + e];
+  a.mid[(int64_t)y * a.params + e] = s;
+}
+
+// Pass 2: G[e] = sum over the slices in order.  The last block instead sums
+// the loss partials: thread t adds partials t, t + 256, ... in order, then a
+// fixed tree over the 256 threads.
+__global__ __launch_bounds__(256) void reduce2_kernel(const ReduceArgs a) {
+  if (blockIdx.x == gridDim.x - 1) {
+    __shared__ float part[256];
+    float s = 0.f;
+    for (int i = threadIdx.x; i < a.nloss; i += 256) s += a.lossPart[i];
+    part[threadIdx.x] = s;
+    __syncthreads();
+    for (int h = 128; h > 0; h >>= 1) {
+      if ((int)threadIdx.x < h) part[threadIdx.x] += part[threadIdx.x + h];
+      __syncthreads();
+    }
+    if (threadIdx.x == 0 && a.loss != nullptr) *a.loss = part[0] * a.loss_scale;
+    return;
+  }
   const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (e < a.params) {
     float s = 0.f;
-    for (int p = 0; p < a.P; ++p) s += a.partial[(int64_t)p * a.params + e];
+#pragma unroll
+    for (int y = 0; y < kReduceSlices; ++y) s += a.mid[(int64_t)y * a.params + e];
     a.G[e] = s;
-  }
-  if (blockIdx.x == 0 && threadIdx.x == 0 && a.loss != nullptr) {
-    float s = 0.f;
-    for (int i = 0; i < a.nloss; ++i) s += a.lossPart[i];
-    *a.loss = s * a.loss_scale;
   }
 }
 
-// One thread per packed bf16 element: fragment (strip, k-block), lane,
-// slot; see common.h for the two orientations and the contraction orders.
+// One thread per packed bf16 element.  The buffer holds the forward
+// layers 0 .. L-1, then the backward layers 1 .. L-1, each as fragments
+// [strip][k-block][lane][slot]; see common.h for the two orientations and
+// the contraction orders.
 __global__ __launch_bounds__(256) void pack_kernel(const PackArgs a) {
-  const int64_t n = (int64_t)a.strips * a.kblocks * 512;
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (e >= n) return;
+  const int64_t e0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (e0 >= a.total) return;
+  const int Wd = a.width, L = a.L;
+  auto fan_in = [&](int l) { return l == 0 ? a.in_dim : Wd; };
+  auto fan_out = [&](int l) { return l == L - 1 ? a.out_dim : Wd; };
+  // locate the layer and orientation of element e0
+  int64_t e = e0, woff = 0;
+  int dir = 0, l = 0;
+  for (;; ++l) {
+    if (l == L) { dir = 1; l = 1; woff = (int64_t)fan_in(0) * fan_out(0); }
+    if (l >= L) return;  // not reached: e0 < total
+    const int fi = fan_in(l), fo = fan_out(l);
+    const int rows = dir == 0 ? fo : fi, cols = dir == 0 ? fi : fo;
+    const int64_t n = (int64_t)((rows + 15) / 16) * ((cols + 31) / 32) * 512;
+    if (e < n) break;
+    e -= n;
+    woff += (int64_t)fi * fo;
+    if (dir == 1 && l == L - 1) return;
+  }
+  const int fi = fan_in(l), fo = fan_out(l);
+  const int kblocks = dir == 0 ? (fi + 31) / 32 : (fo + 31) / 32;
   const int slot = (int)(e & 7), lane = (int)((e >> 3) & 63);
   const int frag = (int)(e >> 9);
-  const int s = frag / a.kblocks, kb = frag - s * a.kblocks;
+  const int s = frag / kblocks, kb = frag - s * kblocks;
   const int g = lane >> 4, row = 16 * s + (lane & 15);
   int pos;  // contraction index the (g, slot) pair stands for
-  if (a.first)
+  if (dir == 0 && l == 0)
     pos = 32 * kb + 8 * g + slot;
   else
     pos = 32 * kb + (slot < 4 ? 4 * g + slot : 16 + 4 * g + (slot - 4));
-  int f, j;  // W[f][j]
-  if (a.dir == 0) { f = pos; j = row; } else { f = row; j = pos; }
+  int f, j;  // W_l[f][j]
+  if (dir == 0) { f = pos; j = row; } else { f = row; j = pos; }
   uint16_t v = 0;
-  if (f < a.fan_in && j < a.fan_out) v = a.W[(int64_t)f * a.fan_out + j];
-  a.dst[e] = v;
+  if (f < fi && j < fo) v = a.W[woff + (int64_t)f * fo + j];
+  a.dst[e0] = v;
 }
 
 template <int W>
@@ -249,14 +367,16 @@ hipError_t launch_wgrad(int width, const WgradArgs& a, hipStream_t s) {
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s) {
   int64_t blocks = (a.params + 255) / 256;
   if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(reduce_kernel, dim3((unsigned)blocks), dim3(256), 0, s, a);
+  hipLaunchKernelGGL(reduce1_kernel, dim3((unsigned)blocks, kReduceSlices), dim3(256), 0, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(reduce2_kernel, dim3((unsigned)blocks + 1), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 hipError_t launch_pack(const PackArgs& a, hipStream_t s) {
-  const int64_t n = (int64_t)a.strips * a.kblocks * 512;
-  if (n == 0) return hipSuccess;
-  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, a);
+  if (a.total == 0) return hipSuccess;
+  hipLaunchKernelGGL(pack_kernel, dim3((unsigned)((a.total + 255) / 256)), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
