@@ -27,6 +27,7 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
   const int L = a.L, out_dim = a.out_dim, out_act = a.out_act;
   const int64_t M = a.M;
   const int SO = (out_dim + 15) >> 4;
+  const int OP = SO * 16;
   const int KBO = (SO + 1) >> 1;
   const bool yvec = (out_dim & 3) == 0;
 
@@ -36,62 +37,76 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
   }
   for (int tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
     const int64_t tb0 = ((int64_t)tile * NW + wave) * NT;
-    u32x4 d[NT][KBW];
+    const int64_t row0 = tb0 * 16;
+    int64_t vrows = M - row0;  // valid rows of this wave's tile
+    vrows = vrows < 0 ? 0 : (vrows > NT * 16 ? NT * 16 : vrows);
+    const int vblk = (int)((vrows + 15) / 16);
+    u32x4 dA[NT][KBW], dB[NT][KBW];
 #pragma unroll
     for (int n = 0; n < NT; ++n)
 #pragma unroll
-      for (int kb = 0; kb < KBW; ++kb) d[n][kb] = u32x4{0u, 0u, 0u, 0u};
+      for (int kb = 0; kb < KBW; ++kb) dA[n][kb] = u32x4{0u, 0u, 0u, 0u};
 
     // Output delta, in chain order.
-    static_for<0, SW>([&](auto sc) {
-      constexpr int s = decltype(sc)::value;
-      if (s >= SO) return;
+    {
+      const rsrc_t dr = make_rsrc(a.deltaOut + row0 * OP, (int64_t)vblk * 32 * OP);
+      const rsrc_t cr = make_rsrc(a.cOut + row0 * OP, a.cOut ? (int64_t)vblk * 64 * OP : 0);
+      const rsrc_t gr = make_rsrc(a.dY + row0 * out_dim, a.dY ? vrows * out_dim * 4 : 0);
+      static_for<0, SW>([&](auto sc) {
+        constexpr int s = decltype(sc)::value;
+        if (s >= SO) return;
 #pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        const int64_t t16 = tb0 + n;
-        uint32_t p0 = 0u, p1 = 0u;
-        if (t16 * 16 < M) {
-          const size_t idx = ((size_t)(t16 * SO + s) * 64 + lane) * 4;
+        for (int n = 0; n < NT; ++n) {
+          const uint32_t so = (uint32_t)((n * SO + s) * 512);
+          uint32_t p0, p1;
           if constexpr (!SEEDED) {
-            const u32x2 v = *reinterpret_cast<const u32x2*>(a.deltaOut + idx);
+            const u32x2 v = bload64(dr, lane * 8, so);
             p0 = v.x;
             p1 = v.y;
           } else {
-            const int64_t m = t16 * 16 + li;
+            const int64_t m = row0 + n * 16 + li;
             const int j0 = s * 16 + lg * 4;
+            const bool ok = m < M && j0 < out_dim;
             float g[4] = {0.f, 0.f, 0.f, 0.f};
-            if (m < M && j0 < out_dim) {
-              const float* dr = a.dY + m * out_dim + j0;
-              if (yvec) {
-                const f32x4 v = *reinterpret_cast<const f32x4*>(dr);
-                g[0] = v[0]; g[1] = v[1]; g[2] = v[2]; g[3] = v[3];
-              } else {
+            if (yvec) {
+              const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
+              const u32x4 v = bload128(gr, eo * 4, (uint32_t)(n * 64 * out_dim));
+              g[0] = __uint_as_float(v.x);
+              g[1] = __uint_as_float(v.y);
+              g[2] = __uint_as_float(v.z);
+              g[3] = __uint_as_float(v.w);
+            } else if (ok) {
+              const float* dp = a.dY + m * out_dim + j0;
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                  if (j0 + r < out_dim) g[r] = dr[r];
-              }
+              for (int r = 0; r < 4; ++r)
+                if (j0 + r < out_dim) g[r] = dp[r];
             }
             if (out_act != ACT_LINEAR) {
-              const f32x4 c = *reinterpret_cast<const f32x4*>(a.cOut + idx);
+              const u32x4 cv = bload128(cr, lane * 16, (uint32_t)((n * SO + s) * 1024));
+              const float c[4] = {__uint_as_float(cv.x), __uint_as_float(cv.y),
+                                  __uint_as_float(cv.z), __uint_as_float(cv.w)};
 #pragma unroll
               for (int r = 0; r < 4; ++r) g[r] *= act_out_grad(out_act, c[r], act_apply(out_act, c[r]));
             }
             p0 = pack_bf16x2(g[0], g[1]);
             p1 = pack_bf16x2(g[2], g[3]);
-            *reinterpret_cast<u32x2*>(a.deltaOut + idx) = u32x2{p0, p1};
+            bstore64(u32x2{p0, p1}, dr, lane * 8, so);
+          }
+          if (s & 1) {
+            dA[n][s >> 1].z = p0;
+            dA[n][s >> 1].w = p1;
+          } else {
+            dA[n][s >> 1].x = p0;
+            dA[n][s >> 1].y = p1;
           }
         }
-        if (s & 1) {
-          d[n][s >> 1].z = p0;
-          d[n][s >> 1].w = p1;
-        } else {
-          d[n][s >> 1].x = p0;
-          d[n][s >> 1].y = p1;
-        }
-      }
-    });
+      });
+    }
 
-    for (int l = L - 1; l >= 1; --l) {
+    // Backward layer l: out = bf16((in W_l^T) * sigma'(a_l)), the delta of
+    // layer l-1 in chain order; it is also stored for the gradient kernel.
+    // The derivative source of strip s is requested PF strips ahead.
+    auto layer = [&](int l, const u32x4 (&in)[NT][KBW], u32x4 (&out)[NT][KBW]) {
       const int KB = (l == L - 1) ? KBO : KBW;
       const uint32_t off = (uint32_t)(l - 1) * a.layH_frags;
       const u32x4* wl;
@@ -103,26 +118,29 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
         __syncthreads();
         wl = smem;
       }
-      const uint16_t* gsrc = (ACT == ACT_SINE ? a.stashS : a.stashA) + (size_t)(l - 1) * a.M16 * W;
-      uint16_t* dst = a.deltaH + (size_t)(l - 1) * a.M16 * W;
-      u32x4 nxt[NT][KBW];
+      const size_t toff = (size_t)(l - 1) * a.M16 * W + (size_t)row0 * W;
+      const rsrc_t gsrc = make_rsrc((ACT == ACT_SINE ? a.stashS : a.stashA) + toff, (int64_t)vblk * 32 * W);
+      const rsrc_t dst = make_rsrc(a.deltaH + toff, (int64_t)vblk * 32 * W);
+      if constexpr (SW == 1) {
 #pragma unroll
-      for (int n = 0; n < NT; ++n)
+        for (int n = 0; n < NT; ++n) {
+          out[n][0].z = 0u;
+          out[n][0].w = 0u;
+        }
+      }
+      constexpr int PF = SW < 4 ? SW : 4;
+      u32x2 gv[SW][NT];
+      auto request = [&](int s) {
+        if constexpr (ACT != ACT_LINEAR) {
 #pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) nxt[n][kb] = u32x4{0u, 0u, 0u, 0u};
+          for (int n = 0; n < NT; ++n) gv[s][n] = bload64(gsrc, lane * 8, (uint32_t)((n * SW + s) * 512));
+        }
+      };
+      static_for<0, PF>([&](auto sc) { request(decltype(sc)::value); });
 
       static_for<0, SW>([&](auto sc) {
         constexpr int s = decltype(sc)::value;
-        u32x2 gv[NT];
-        if constexpr (ACT != ACT_LINEAR) {
-#pragma unroll
-          for (int n = 0; n < NT; ++n) {
-            const int64_t t16 = tb0 + n;
-            gv[n] = (t16 * 16 < M)
-                        ? *reinterpret_cast<const u32x2*>(gsrc + ((size_t)(t16 * SW + s) * 64 + lane) * 4)
-                        : u32x2{0u, 0u};
-          }
-        }
+        if constexpr (s + PF < SW) request(s + PF);
         u32x4 af[KBW];
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb)
@@ -134,40 +152,46 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
         for (int kb = 0; kb < KBW; ++kb) {
           if (kb < KB) {
 #pragma unroll
-            for (int n = 0; n < NT; ++n) acc[n] = mfma16(af[kb], d[n][kb], acc[n]);
+            for (int n = 0; n < NT; ++n) acc[n] = mfma16(af[kb], in[n][kb], acc[n]);
           }
         }
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
-          float dd[4];
-          if constexpr (ACT != ACT_LINEAR) {
-            dd[0] = acc[n][0] * act_hidden_grad<ACT>(bf16_lo(gv[n].x));
-            dd[1] = acc[n][1] * act_hidden_grad<ACT>(bf16_hi(gv[n].x));
-            dd[2] = acc[n][2] * act_hidden_grad<ACT>(bf16_lo(gv[n].y));
-            dd[3] = acc[n][3] * act_hidden_grad<ACT>(bf16_hi(gv[n].y));
+          uint32_t p0, p1;
+          if constexpr (ACT == ACT_RELU) {
+            // relu'(a) is [a > 0]; zero the rounded products where a is 0
+            p0 = mask_bf16x2_by_positive(pack_bf16x2(acc[n][0], acc[n][1]), gv[s][n].x);
+            p1 = mask_bf16x2_by_positive(pack_bf16x2(acc[n][2], acc[n][3]), gv[s][n].y);
+          } else if constexpr (ACT == ACT_LINEAR) {
+            p0 = pack_bf16x2(acc[n][0], acc[n][1]);
+            p1 = pack_bf16x2(acc[n][2], acc[n][3]);
           } else {
-            dd[0] = acc[n][0]; dd[1] = acc[n][1]; dd[2] = acc[n][2]; dd[3] = acc[n][3];
+            p0 = pack_bf16x2(acc[n][0] * act_hidden_grad<ACT>(bf16_lo(gv[s][n].x)),
+                             acc[n][1] * act_hidden_grad<ACT>(bf16_hi(gv[s][n].x)));
+            p1 = pack_bf16x2(acc[n][2] * act_hidden_grad<ACT>(bf16_lo(gv[s][n].y)),
+                             acc[n][3] * act_hidden_grad<ACT>(bf16_hi(gv[s][n].y)));
           }
-          const uint32_t p0 = pack_bf16x2(dd[0], dd[1]), p1 = pack_bf16x2(dd[2], dd[3]);
-          if (s & 1) {
-            nxt[n][s >> 1].z = p0;
-            nxt[n][s >> 1].w = p1;
+          if constexpr (s & 1) {
+            out[n][s >> 1].z = p0;
+            out[n][s >> 1].w = p1;
           } else {
-            nxt[n][s >> 1].x = p0;
-            nxt[n][s >> 1].y = p1;
+            out[n][s >> 1].x = p0;
+            out[n][s >> 1].y = p1;
           }
-          const int64_t t16 = tb0 + n;
-          if (t16 * 16 < M)
-            *reinterpret_cast<u32x2*>(dst + ((size_t)(t16 * SW + s) * 64 + lane) * 4) = u32x2{p0, p1};
+          bstore64(u32x2{p0, p1}, dst, lane * 8, (uint32_t)((n * SW + s) * 512));
         }
         // Keep each strip's work together: bounds the live registers.
         __builtin_amdgcn_sched_barrier(0);
       });
-#pragma unroll
-      for (int n = 0; n < NT; ++n)
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) d[n][kb] = nxt[n][kb];
+    };
+
+    // Layers in pairs with two delta buffers, so no register array is copied.
+    int l = L - 1;
+    for (; l - 2 >= 0; l -= 2) {
+      layer(l, dA, dB);
+      layer(l - 1, dB, dA);
     }
+    if (l >= 1) layer(l, dA, dB);
   }
 }
 

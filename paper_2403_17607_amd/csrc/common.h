@@ -69,12 +69,12 @@ inline int tile_rows(int width) {
 // 16x16 output tiles; GK x GJ blocks cover G; KS waves split every chunk of
 // the batch; each wave runs KSW 32-row contraction steps per chunk.
 template <int W> struct WgCfg;
-// The chunk is CH = 32 KS KSW rows, so CH * W / 8 = 1024 16-byte units per
-// tensor at every width (four per thread).
-template <> struct WgCfg<16> { static constexpr int TBK = 1, TBJ = 1, GK = 1, GJ = 1, KS = 4, KSW = 4; };
-template <> struct WgCfg<32> { static constexpr int TBK = 2, TBJ = 2, GK = 1, GJ = 1, KS = 4, KSW = 2; };
-template <> struct WgCfg<64> { static constexpr int TBK = 2, TBJ = 2, GK = 2, GJ = 2, KS = 1, KSW = 4; };
-template <> struct WgCfg<128> { static constexpr int TBK = 4, TBJ = 4, GK = 2, GJ = 2, KS = 1, KSW = 2; };
+// The chunk is CH = 32 KS KSW rows, so CH * W / 8 = 2048 16-byte units per
+// tensor at every width (eight per thread, all in flight at once).
+template <> struct WgCfg<16> { static constexpr int TBK = 1, TBJ = 1, GK = 1, GJ = 1, KS = 4, KSW = 8; };
+template <> struct WgCfg<32> { static constexpr int TBK = 2, TBJ = 2, GK = 1, GJ = 1, KS = 4, KSW = 4; };
+template <> struct WgCfg<64> { static constexpr int TBK = 2, TBJ = 2, GK = 2, GJ = 2, KS = 1, KSW = 8; };
+template <> struct WgCfg<128> { static constexpr int TBK = 4, TBJ = 4, GK = 2, GJ = 2, KS = 1, KSW = 4; };
 template <int W> constexpr int wg_chunk() { return 32 * WgCfg<W>::KS * WgCfg<W>::KSW; }
 inline int wgrad_chunk(int width) {
   switch (width) {

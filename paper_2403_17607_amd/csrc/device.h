@@ -25,6 +25,26 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, r);
 }
 
+// ReLU of two packed bf16 values: a bf16 value is <= 0 exactly when its bit
+// pattern read as int16 is <= 0, so a packed int16 max with 0 is ReLU.  It
+// commutes with rounding (rounding keeps the sign), so ReLU may be applied
+// after the conversion.
+typedef short s16x2 __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ uint32_t relu_bf16x2(uint32_t p) {
+  return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, p), (s16x2){0, 0}));
+}
+
+// Zero each bf16 half of p whose half in a is zero (a holds non-negative bf16
+// values, so "nonzero" is "> 0").  Two packed int16 instructions.
+__device__ __forceinline__ uint32_t mask_bf16x2_by_positive(uint32_t p, uint32_t a) {
+  // the constant 1 in both halves comes from a register: an inline
+  // constant of a packed instruction would give the high half 0
+  uint32_t m, r;
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(m) : "v"(a), "v"(0x00010001u));
+  asm("v_pk_mul_lo_u16 %0, %1, %2" : "=v"(r) : "v"(p), "v"(m));
+  return r;
+}
+
 __device__ __forceinline__ float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ __forceinline__ float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xffff0000u); }
 
@@ -72,6 +92,30 @@ __device__ __forceinline__ float act_hidden(float c) {
   else if constexpr (ACT == ACT_SIGMOID) return 1.f / (1.f + __expf(-c));
   else if constexpr (ACT == ACT_SINE) return __sinf(c);
   else return c;
+}
+
+// Buffer descriptor over [base, base + bytes) (gfx9 raw buffer, no
+// swizzle).  The hardware range check makes loads past the end return 0 and
+// drops stores past the end, so a wave can address its whole tile with
+// 32-bit offsets and no per-row branches.
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+constexpr uint32_t kOOB = 0x80000000u;  // an offset past any descriptor's end
+
+__device__ __forceinline__ rsrc_t make_rsrc(const void* base, int64_t bytes) {
+  const int n = bytes <= 0 ? 0 : (bytes > 0x7fffffff ? 0x7fffffff : (int)bytes);
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, n, 0x00020000);
+}
+__device__ __forceinline__ u32x2 bload64(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r, voff, soff, 0));
+}
+__device__ __forceinline__ u32x4 bload128(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ void bstore64(u32x2 v, rsrc_t r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, 0);
+}
+__device__ __forceinline__ void bstore128(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, 0);
 }
 
 // Cooperative copy of nfrag 1 KiB fragments from global memory into LDS.

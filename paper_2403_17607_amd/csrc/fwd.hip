@@ -9,21 +9,28 @@
 // from LDS as the A operand.  When every layer's packed weights fit in LDS
 // they are loaded once per workgroup; otherwise each layer is staged in
 // turn (section III-B stages one weight matrix at a time in shared local
-// memory).  HBM is touched for X, Y and, when training, the stash.
+// memory).  HBM is touched for X, Y and, when training, T and the stash.
+//
+// The weight fragments of the next strip are read from LDS while the
+// current strip's MFMAs run (across the layer boundary too when all layers
+// are resident).  Global memory is addressed through one buffer descriptor
+// per wave tile, whose range check replaces per-row bounds branches.
 #include "device.h"
 
 namespace ffmlp {
 
-// acc[n] = (packed strip s of the layer) x act[n]: one 16-feature strip of
-// C^T for the NT 16-row blocks of the wave, KB k-blocks deep.
-template <int NT, int KBW>
-__device__ __forceinline__ void strip_product(const u32x4* wl, int s, int KB,
-                                              const u32x4 (&act)[NT][KBW], f32x4 (&acc)[NT],
-                                              int lane) {
-  u32x4 af[KBW];
+template <int KBW>
+__device__ __forceinline__ void load_frags(const u32x4* wl, int s, int KB, int lane,
+                                           u32x4 (&af)[KBW]) {
 #pragma unroll
   for (int kb = 0; kb < KBW; ++kb)
     af[kb] = (kb < KB) ? wl[(s * KB + kb) * 64 + lane] : u32x4{0u, 0u, 0u, 0u};
+}
+
+// acc[n] = (one 16-feature strip of the packed layer) x act[n], KB k-blocks.
+template <int NT, int KBW>
+__device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], int KB,
+                                              const u32x4 (&act)[NT][KBW], f32x4 (&acc)[NT]) {
 #pragma unroll
   for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
@@ -48,151 +55,195 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
   const int64_t M = a.M;
   const int KB0 = (in_dim + 31) >> 5;
   const int SO = (out_dim + 15) >> 4;
+  const int OP = SO * 16;
   const bool xvec = (in_dim & 7) == 0;
   const bool yvec = (out_dim & 3) == 0;
   const int out_act = a.out_act;
+  const bool resident = a.resident != 0;
+  auto layer_off = [&](int l) -> uint32_t {
+    return l == 0 ? 0u : a.lay0_frags + (uint32_t)(l - 1) * a.layH_frags;
+  };
 
-  if (a.resident) {
+  if (resident) {
     copy_frags(smem, a.packed, a.total_frags, tid, NTH);
     __syncthreads();
   }
   float loss = 0.f;
   for (int tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
     const int64_t tb0 = ((int64_t)tile * NW + wave) * NT;  // first 16-row block
-    u32x4 act[NT][KBW];
+    const int64_t row0 = tb0 * 16;
+    int64_t vrows = M - row0;  // valid rows of this wave's tile
+    vrows = vrows < 0 ? 0 : (vrows > NT * 16 ? NT * 16 : vrows);
+    const int vblk = (int)((vrows + 15) / 16);
+
+    // Two activation buffers and two weight-fragment buffers, used in turn
+    // (hidden layers go in pairs), so no register array is ever copied.
+    u32x4 actA[NT][KBW], actB[NT][KBW];
+    u32x4 afb[2][KBW];
+    if (resident && L > 1) load_frags<KBW>(smem, 0, KB0, lane, afb[0]);
+
     // A_1 = X in input order: lane group g takes features 32 kb + 8 g .. + 7.
-#pragma unroll
-    for (int n = 0; n < NT; ++n) {
-      const int64_t m = (tb0 + n) * 16 + li;
+    if (xvec) {
+      // per-lane byte offset inside a 16-row block; the block goes in the
+      // scalar offset
+      const rsrc_t xr = make_rsrc(a.X + row0 * in_dim, vrows * in_dim * 2);
 #pragma unroll
       for (int kb = 0; kb < KBW; ++kb) {
-        u32x4 v = {0u, 0u, 0u, 0u};
         const int f0 = kb * 32 + lg * 8;
-        if (kb < KB0 && m < M && f0 < in_dim) {
-          const uint16_t* xr = a.X + m * in_dim + f0;
-          if (xvec) {
-            v = *reinterpret_cast<const u32x4*>(xr);
-          } else {
-            uint32_t e[8];
+        const uint32_t voff = (kb < KB0 && f0 < in_dim) ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
+#pragma unroll
+        for (int n = 0; n < NT; ++n) actA[n][kb] = bload128(xr, voff, (uint32_t)(n * 32 * in_dim));
+      }
+    } else {
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const int64_t m = row0 + n * 16 + li;
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+          const int f0 = kb * 32 + lg * 8;
+          uint32_t e[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+          if (kb < KB0 && m < M && f0 < in_dim) {
+            const uint16_t* xr = a.X + m * in_dim + f0;
 #pragma unroll
             for (int q = 0; q < 8; ++q) e[q] = (f0 + q < in_dim) ? (uint32_t)xr[q] : 0u;
-            v = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
-                      e[6] | (e[7] << 16)};
           }
+          actA[n][kb] = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
+                              e[6] | (e[7] << 16)};
         }
-        act[n][kb] = v;
       }
     }
 
-    // Hidden layers: A_{l+1} = bf16(sigma(A_l W_l)), kept in registers.
-    for (int l = 0; l < L - 1; ++l) {
+    // Hidden layer l: out = bf16(sigma(in W_l)) in the next layer's chain
+    // order (see common.h).  P is the layer's parity within its pair; the
+    // fragment buffer of strip s is (P * SW + s) % 2.
+    auto hidden = [&](auto Pc, int l, const u32x4 (&in)[NT][KBW], u32x4 (&out)[NT][KBW]) {
+      constexpr int P = decltype(Pc)::value;
       const int KB = (l == 0) ? KB0 : KBW;
-      const uint32_t off = (l == 0) ? 0u : a.lay0_frags + (uint32_t)(l - 1) * a.layH_frags;
       const u32x4* wl;
-      if (a.resident) {
-        wl = smem + (size_t)off * 64;
+      if (resident) {
+        wl = smem + (size_t)layer_off(l) * 64;
       } else {
         __syncthreads();
-        copy_frags(smem, a.packed + (size_t)off * 64, (uint32_t)(SW * KB), tid, NTH);
+        copy_frags(smem, a.packed + (size_t)layer_off(l) * 64, (uint32_t)(SW * KB), tid, NTH);
         __syncthreads();
         wl = smem;
+        load_frags<KBW>(wl, 0, KB, lane, afb[(P * SW) & 1]);
       }
-      u32x4 nxt[NT][KBW];
-#pragma unroll
-      for (int n = 0; n < NT; ++n)
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) nxt[n][kb] = u32x4{0u, 0u, 0u, 0u};
-
-      static_for<0, SW>([&](auto sc) {
-        constexpr int s = decltype(sc)::value;
-        f32x4 acc[NT];
-        strip_product<NT, KBW>(wl, s, KB, act, acc, lane);
-        // Placed in the next layer's chain order (see common.h).
+      const size_t soff = (size_t)l * a.M16 * W + (size_t)row0 * W;
+      const rsrc_t sa = make_rsrc(a.stashA + soff, a.stashA ? (int64_t)vblk * 32 * W : 0);
+      const rsrc_t ss = make_rsrc(a.stashS + soff, a.stashS ? (int64_t)vblk * 32 * W : 0);
+      if constexpr (SW == 1) {
+        // width 16: the second half of the only k-block is padding
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
-          const uint32_t p0 = pack_bf16x2(act_hidden<ACT>(acc[n][0]), act_hidden<ACT>(acc[n][1]));
-          const uint32_t p1 = pack_bf16x2(act_hidden<ACT>(acc[n][2]), act_hidden<ACT>(acc[n][3]));
-          if (s & 1) {
-            nxt[n][s >> 1].z = p0;
-            nxt[n][s >> 1].w = p1;
+          out[n][0].z = 0u;
+          out[n][0].w = 0u;
+        }
+      }
+      static_for<0, SW>([&](auto sc) {
+        constexpr int s = decltype(sc)::value;
+        constexpr int cur = (P * SW + s) & 1;
+        if constexpr (s + 1 < SW) {
+          load_frags<KBW>(wl, s + 1, KB, lane, afb[cur ^ 1]);
+        } else {
+          if (resident && l + 1 < L - 1)
+            load_frags<KBW>(smem + (size_t)layer_off(l + 1) * 64, 0, KBW, lane, afb[cur ^ 1]);
+        }
+        f32x4 acc[NT];
+        strip_product<NT, KBW>(afb[cur], KB, in, acc);
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+          uint32_t p0, p1;
+          if constexpr (ACT == ACT_RELU) {
+            p0 = relu_bf16x2(pack_bf16x2(acc[n][0], acc[n][1]));
+            p1 = relu_bf16x2(pack_bf16x2(acc[n][2], acc[n][3]));
           } else {
-            nxt[n][s >> 1].x = p0;
-            nxt[n][s >> 1].y = p1;
+            p0 = pack_bf16x2(act_hidden<ACT>(acc[n][0]), act_hidden<ACT>(acc[n][1]));
+            p1 = pack_bf16x2(act_hidden<ACT>(acc[n][2]), act_hidden<ACT>(acc[n][3]));
+          }
+          if constexpr (s & 1) {
+            out[n][s >> 1].z = p0;
+            out[n][s >> 1].w = p1;
+          } else {
+            out[n][s >> 1].x = p0;
+            out[n][s >> 1].y = p1;
           }
           if constexpr (MODE != FWD_INFER) {
-            const int64_t t16 = tb0 + n;
-            if (t16 * 16 < M) {
-              const size_t idx = (size_t)l * a.M16 * W + ((size_t)(t16 * SW + s) * 64 + lane) * 4;
-              *reinterpret_cast<u32x2*>(a.stashA + idx) = u32x2{p0, p1};
-              if constexpr (ACT == ACT_SINE) {
-                const uint32_t c0 = pack_bf16x2(__cosf(acc[n][0]), __cosf(acc[n][1]));
-                const uint32_t c1 = pack_bf16x2(__cosf(acc[n][2]), __cosf(acc[n][3]));
-                *reinterpret_cast<u32x2*>(a.stashS + idx) = u32x2{c0, c1};
-              }
+            const uint32_t so = (uint32_t)((n * SW + s) * 512);
+            bstore64(u32x2{p0, p1}, sa, lane * 8, so);
+            if constexpr (ACT == ACT_SINE) {
+              const uint32_t c0 = pack_bf16x2(__cosf(acc[n][0]), __cosf(acc[n][1]));
+              const uint32_t c1 = pack_bf16x2(__cosf(acc[n][2]), __cosf(acc[n][3]));
+              bstore64(u32x2{c0, c1}, ss, lane * 8, so);
             }
           }
         }
         // Keep each strip's work together: bounds the live registers.
         __builtin_amdgcn_sched_barrier(0);
       });
-#pragma unroll
-      for (int n = 0; n < NT; ++n)
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) act[n][kb] = nxt[n][kb];
-    }
+    };
 
     // Output layer: Y = sigma_out(C_L); when training also the loss and the
     // output delta 2 (Y - T) / (M out_dim) * sigma_out'(C_L).
-    {
+    auto output = [&](const u32x4 (&in)[NT][KBW]) {
       const int l = L - 1;
       const int KB = (l == 0) ? KB0 : KBW;
-      const uint32_t off = (l == 0) ? 0u : a.lay0_frags + (uint32_t)(l - 1) * a.layH_frags;
       const u32x4* wl;
-      if (a.resident) {
-        wl = smem + (size_t)off * 64;
+      if (resident) {
+        wl = smem + (size_t)layer_off(l) * 64;
       } else {
         __syncthreads();
-        copy_frags(smem, a.packed + (size_t)off * 64, (uint32_t)(SO * KB), tid, NTH);
+        copy_frags(smem, a.packed + (size_t)layer_off(l) * 64, (uint32_t)(SO * KB), tid, NTH);
         __syncthreads();
         wl = smem;
       }
+      const rsrc_t yr = make_rsrc(a.Y + row0 * out_dim, a.Y ? vrows * out_dim * 2 : 0);
+      const rsrc_t tr = make_rsrc(a.T + row0 * out_dim, a.T ? vrows * out_dim * 4 : 0);
+      const rsrc_t dr = make_rsrc(a.deltaOut + row0 * OP, a.deltaOut ? (int64_t)vblk * 32 * OP : 0);
+      const rsrc_t cr = make_rsrc(a.cOut + row0 * OP, a.cOut ? (int64_t)vblk * 64 * OP : 0);
       for (int s = 0; s < SO; ++s) {
+        u32x4 af[KBW];
+        load_frags<KBW>(wl, s, KB, lane, af);
         f32x4 acc[NT];
-        strip_product<NT, KBW>(wl, s, KB, act, acc, lane);
+        strip_product<NT, KBW>(af, KB, in, acc);
+        const int j0 = s * 16 + lg * 4;
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
-          const int64_t t16 = tb0 + n;
-          const int64_t m = t16 * 16 + li;
-          const int j0 = s * 16 + lg * 4;
+          const int64_t m = row0 + n * 16 + li;
           const bool ok = (m < M) && (j0 < out_dim);
+          // element offset of (row li, j0) inside the block (past the end if
+          // the column is); the block's offset goes in the scalar offset
+          const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
+          const uint32_t bo = (uint32_t)(n * 16 * out_dim);
           float y[4];
 #pragma unroll
           for (int r = 0; r < 4; ++r) y[r] = act_apply(out_act, acc[n][r]);
           const uint32_t y0 = pack_bf16x2(y[0], y[1]), y1 = pack_bf16x2(y[2], y[3]);
-          if (a.Y != nullptr && ok) {
-            uint16_t* yr = a.Y + m * out_dim + j0;
+          if (a.Y != nullptr) {
             if (yvec) {
-              *reinterpret_cast<u32x2*>(yr) = u32x2{y0, y1};
-            } else {
+              bstore64(u32x2{y0, y1}, yr, eo * 2, bo * 2);
+            } else if (ok) {
+              uint16_t* yp = a.Y + m * out_dim + j0;
               const uint16_t yb[4] = {(uint16_t)(y0 & 0xffff), (uint16_t)(y0 >> 16),
                                       (uint16_t)(y1 & 0xffff), (uint16_t)(y1 >> 16)};
 #pragma unroll
               for (int r = 0; r < 4; ++r)
-                if (j0 + r < out_dim) yr[r] = yb[r];
+                if (j0 + r < out_dim) yp[r] = yb[r];
             }
           }
           if constexpr (MODE == FWD_TRAIN) {
             float t[4] = {0.f, 0.f, 0.f, 0.f};
-            if (ok) {
-              const float* tr = a.T + m * out_dim + j0;
-              if (yvec) {
-                const f32x4 tv = *reinterpret_cast<const f32x4*>(tr);
-                t[0] = tv[0]; t[1] = tv[1]; t[2] = tv[2]; t[3] = tv[3];
-              } else {
+            if (yvec) {
+              const u32x4 tv = bload128(tr, eo * 4, bo * 4);
+              t[0] = __uint_as_float(tv.x);
+              t[1] = __uint_as_float(tv.y);
+              t[2] = __uint_as_float(tv.z);
+              t[3] = __uint_as_float(tv.w);
+            } else if (ok) {
+              const float* tp = a.T + m * out_dim + j0;
 #pragma unroll
-                for (int r = 0; r < 4; ++r)
-                  if (j0 + r < out_dim) t[r] = tr[r];
-              }
+              for (int r = 0; r < 4; ++r)
+                if (j0 + r < out_dim) t[r] = tp[r];
             }
             float d[4];
 #pragma unroll
@@ -202,20 +253,27 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
               if (valid) loss += diff * diff;
               d[r] = valid ? (a.scale * diff) * act_out_grad(out_act, acc[n][r], y[r]) : 0.f;
             }
-            if (t16 * 16 < M) {
-              const size_t idx = ((size_t)(t16 * SO + s) * 64 + lane) * 4;
-              *reinterpret_cast<u32x2*>(a.deltaOut + idx) =
-                  u32x2{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])};
-            }
+            bstore64(u32x2{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])}, dr, lane * 8,
+                     (uint32_t)((n * SO + s) * 512));
           }
           if constexpr (MODE == FWD_STASH) {
-            if (a.cOut != nullptr && t16 * 16 < M) {
-              const size_t idx = ((size_t)(t16 * SO + s) * 64 + lane) * 4;
-              *reinterpret_cast<f32x4*>(a.cOut + idx) = acc[n];
-            }
+            bstore128(__builtin_bit_cast(u32x4, acc[n]), cr, lane * 16,
+                      (uint32_t)((n * SO + s) * 1024));
           }
         }
       }
+    };
+
+    int l = 0;
+    for (; l + 2 <= L - 1; l += 2) {
+      hidden(std::integral_constant<int, 0>{}, l, actA, actB);
+      hidden(std::integral_constant<int, 1>{}, l + 1, actB, actA);
+    }
+    if (l < L - 1) {
+      hidden(std::integral_constant<int, 0>{}, l, actA, actB);
+      output(actB);
+    } else {
+      output(actA);
     }
   }
 

@@ -55,10 +55,13 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
 
   u32x4 ra[UPT], rd[UPT];
 
-  // ---- global -> registers ----
-  // The loads are unconditional (an out-of-range unit reads the tensor's
-  // first 16 bytes instead) so that all of a chunk's loads are in flight
-  // together; rows past M are zeroed when the registers go to LDS.
+  // ---- global -> registers: buffer loads ----
+  // A chunk of a tensor is read through a buffer descriptor whose base is
+  // the chunk's first byte and whose size is the chunk's valid bytes; the
+  // hardware returns zeros past that size, which covers rows past the
+  // batch.  (Stash rows between M and the next multiple of 16 hold finite
+  // activations and exactly zero deltas, so they add nothing to G.)  The
+  // per-unit byte offsets do not depend on the chunk and are computed once.
   //
   // Tile-image tensor with F features: unit v covers rows 16 tl + 2 ip,
   // +1 and features 16 s + 4 g + 0..3.  Consecutive lanes take consecutive
@@ -72,34 +75,56 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
     const int g = rest2 & 3, rest3 = rest2 >> 2;
     return TileUnit{(rest3 / S) * 4 + tla, rest3 % S, g, ip};
   };
-  auto addr_tile = [&](const uint16_t* (&pa)[UPT], const uint16_t* src, int F, int64_t c0) {
-    const int S = F >> 4;
-    const int U = CH * F / 8;
+  // Byte offset of unit v inside the chunk (past the chunk when v >= U).
+  auto tile_voff = [&](int v, int S) {
+    const TileUnit t = tile_unit(v, S);
+    return (uint32_t)((((t.tl * S + t.s) * 4 + t.g) * 8 + t.ip) * 16);
+  };
+  const bool xmode = (l == 0);
+  uint32_t voa[UPT], vod[UPT];
+  {
+    const int SA = W / 16, SD = dF / 16;
 #pragma unroll
     for (int k = 0; k < UPT; ++k) {
       const int v = k * 256 + tid;
-      const TileUnit t = tile_unit(v, S);
-      const bool ok = v < U && c0 + 16 * t.tl < M;
-      pa[k] = src + (ok ? (size_t)c0 * F + ((size_t)((t.tl * S + t.s) * 4 + t.g) * 8 + t.ip) * 8 : 0);
+      vod[k] = tile_voff(v, SD);  // >= the chunk size when v is past it
+      voa[k] = tile_voff(v, SA);
     }
-  };
-  // X (row-major [M][in_dim], in_dim a multiple of 8): unit pair q covers
-  // rows 2 j, 2 j + 1 and features 8 f8 .. + 7; consecutive lanes take
-  // consecutive j.
-  auto addr_x = [&](const uint16_t* (&pa)[UPT], int64_t c0) {
-    const int npairs = (CH / 2) * nf8;
+    if (xmode) {
+      // X (row-major, in_dim a multiple of 8): unit pair q covers rows
+      // 2 j, 2 j + 1 and features 8 f8 .. + 7; consecutive lanes take
+      // consecutive j.
+      const int npairs = (CH / 2) * nf8;
 #pragma unroll
-    for (int k = 0; k < UPT / 2; ++k) {
-      const int q = k * 256 + tid;
-      const int j = q % (CH / 2), f0 = (q / (CH / 2)) * 8;
-      const int64_t row = c0 + 2 * j;
-      const bool ok0 = q < npairs && row < M, ok1 = q < npairs && row + 1 < M;
-      pa[2 * k] = a.X + (ok0 ? row * in_dim + f0 : 0);
-      pa[2 * k + 1] = a.X + (ok1 ? (row + 1) * in_dim + f0 : 0);
+      for (int k = 0; k < UPT / 2; ++k) {
+        const int q = k * 256 + tid;
+        const int j = q % (CH / 2), f0 = (q / (CH / 2)) * 8;
+        const uint32_t past = (uint32_t)(CH * in_dim * 2);
+        voa[2 * k] = q < npairs ? (uint32_t)((2 * j * in_dim + f0) * 2) : past;
+        voa[2 * k + 1] = q < npairs ? (uint32_t)(((2 * j + 1) * in_dim + f0) * 2) : past;
+      }
     }
+  }
+  auto rsrc = [&](const uint16_t* base, int64_t c0, int row_bytes, int64_t rows_valid) {
+    int64_t rows = rows_valid - c0;
+    if (rows > CH) rows = CH;
+    if (rows < 0) rows = 0;
+    return __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(base) + c0 * (row_bytes / 2),
+                                             (short)0, (int)(rows * row_bytes), 0x00020000);
   };
+  auto load_chunk = [&](int64_t c) {
+    const int64_t c0 = c * CH;
+    const __amdgpu_buffer_rsrc_t rd_src = rsrc(dsrc, c0, dF * 2, a.M16);
+    const __amdgpu_buffer_rsrc_t ra_src =
+        xmode ? rsrc(a.X, c0, in_dim * 2, xvec ? M : 0) : rsrc(asrc, c0, W * 2, a.M16);
+#pragma unroll
+    for (int k = 0; k < UPT; ++k) ra[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(ra_src, voa[k], 0, 0));
+#pragma unroll
+    for (int k = 0; k < UPT; ++k) rd[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rd_src, vod[k], 0, 0));
+  };
+
   // ---- registers -> LDS, transposed to [feature][batch row] ----
-  auto store_tile = [&](const u32x4 (&r)[UPT], uint32_t* T32, int F, int64_t c0) {
+  auto store_tile = [&](const u32x4 (&r)[UPT], uint32_t* T32, int F) {
     const int S = F >> 4;
     const int U = CH * F / 8;
 #pragma unroll
@@ -107,10 +132,7 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
       const int v = k * 256 + tid;
       if (v < U) {
         const TileUnit t = tile_unit(v, S);
-        const int64_t row = c0 + 16 * t.tl + 2 * t.ip;
-        u32x4 x = r[k];
-        if (row >= M) { x.x = 0u; x.y = 0u; }
-        if (row + 1 >= M) { x.z = 0u; x.w = 0u; }
+        const u32x4 x = r[k];
         uint32_t* d = T32 + (16 * t.s + 4 * t.g) * LDW + 8 * t.tl + t.ip;
         d[0 * LDW] = (x.x & 0xffffu) | (x.z << 16);
         d[1 * LDW] = (x.x >> 16) | (x.z & 0xffff0000u);
@@ -119,17 +141,14 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
       }
     }
   };
-  auto store_x = [&](const u32x4 (&r)[UPT], int64_t c0) {
+  auto store_x = [&](const u32x4 (&r)[UPT]) {
     const int npairs = (CH / 2) * nf8;
 #pragma unroll
     for (int k = 0; k < UPT / 2; ++k) {
       const int q = k * 256 + tid;
       if (q < npairs) {
         const int j = q % (CH / 2), f0 = (q / (CH / 2)) * 8;
-        const int64_t row = c0 + 2 * j;
-        u32x4 x0 = r[2 * k], x1 = r[2 * k + 1];
-        if (row >= M) x0 = u32x4{0u, 0u, 0u, 0u};
-        if (row + 1 >= M) x1 = u32x4{0u, 0u, 0u, 0u};
+        const u32x4 x0 = r[2 * k], x1 = r[2 * k + 1];
         const uint32_t w0[4] = {x0.x, x0.y, x0.z, x0.w}, w1[4] = {x1.x, x1.y, x1.z, x1.w};
         uint32_t* d = AT32 + f0 * LDW + j;
 #pragma unroll
@@ -138,6 +157,15 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
           d[(2 * e + 1) * LDW] = (w0[e] >> 16) | (w1[e] & 0xffff0000u);
         }
       }
+    }
+  };
+  // Other input widths: X goes straight from global memory into LDS,
+  // element by element, when the chunk is stored (no register staging).
+  auto copy_x_scalar = [&](int64_t c0) {
+    for (int u = tid; u < CH * in_dim; u += 256) {
+      const int ml = u / in_dim, f = u - ml * in_dim;
+      const int64_t row = c0 + ml;
+      AT[(size_t)f * LDT + ml] = row < M ? a.X[row * in_dim + f] : (uint16_t)0;
     }
   };
 
@@ -152,40 +180,13 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   int64_t c_end = c_begin + a.chunks_per_block;
   if (c_end > nch) c_end = nch;
 
-  // Other input widths: X goes straight from global memory into LDS,
-  // element by element, when the chunk is stored (no register staging).
-  auto copy_x_scalar = [&](int64_t c0) {
-    for (int u = tid; u < CH * in_dim; u += 256) {
-      const int ml = u / in_dim, f = u - ml * in_dim;
-      const int64_t row = c0 + ml;
-      AT[(size_t)f * LDT + ml] = row < M ? a.X[row * in_dim + f] : (uint16_t)0;
-    }
-  };
-  // Addresses first (uniform branches), then one unconditional load per
-  // unit, so the loads of a chunk are all in flight together.
-  auto load_chunk = [&](int64_t c) {
-    const uint16_t* pa[UPT];
-    const uint16_t* pd[UPT];
-    if (l != 0) addr_tile(pa, asrc, W, c * CH);
-    else if (xvec) addr_x(pa, c * CH);
-    else {
-#pragma unroll
-      for (int k = 0; k < UPT; ++k) pa[k] = a.X;
-    }
-    addr_tile(pd, dsrc, dF, c * CH);
-#pragma unroll
-    for (int k = 0; k < UPT; ++k) ra[k] = *reinterpret_cast<const u32x4*>(pa[k]);
-#pragma unroll
-    for (int k = 0; k < UPT; ++k) rd[k] = *reinterpret_cast<const u32x4*>(pd[k]);
-  };
-
   if (c_begin < c_end) load_chunk(c_begin);
   for (int64_t c = c_begin; c < c_end; ++c) {
     __syncthreads();  // every wave is done reading the previous chunk
-    if (l != 0) store_tile(ra, AT32, W, c * CH);
-    else if (xvec) store_x(ra, c * CH);
+    if (!xmode) store_tile(ra, AT32, W);
+    else if (xvec) store_x(ra);
     else copy_x_scalar(c * CH);
-    store_tile(rd, DT32, dF, c * CH);
+    store_tile(rd, DT32, dF);
     __syncthreads();
     if (c + 1 < c_end) load_chunk(c + 1);
 #pragma unroll
