@@ -57,6 +57,27 @@ def train_bytes_per_row(width, depth, in_dim, out_dim, act):
     return b
 
 
+def measured_traffic(key):
+    """HBM bytes per launch of the inference kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE runs (profiles/traffic.json), or None
+    when there are none for this workload or the kernel sources have changed
+    since they were taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    entry = json.load(open(path)).get(key)
+    if entry is None:
+        return None
+    h = hashlib.sha256()
+    for src in entry["sources"]:
+        with open(os.path.join(ROOT, src), "rb") as f:
+            h.update(f.read())
+    if h.hexdigest() != entry["sources_sha256"]:
+        return None
+    return entry["hbm_bytes_per_launch"]
+
+
 def cpu_baseline(width, depth, in_dim, out_dim, act, out_act, target_s=12.0):
     """The oracle (fp64, OpenMP over rows) on a bounded sample of the step:
     one inference forward plus one training step per row."""
@@ -197,7 +218,12 @@ def main():
         "event_ms_per_step": t_step,
         "roofline": {"kernel": "fwd_kernel (inference)", "bound": "mfma",
                      "achieved": inf_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": inf_tflops / PEAK_BF16_TFLOPS, "traffic": None,
+                     "frac": inf_tflops / PEAK_BF16_TFLOPS,
+                     "traffic": measured_traffic(
+                         f"fwd_infer_w{width}_d{depth}_in{in_dim}_out{out_dim}_{args.act}_b{M}")
+                     if args.out_act == "linear" else None,
+                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
+                                     "scaled by a reference copy)",
                      "flops_per_row": fl_inf, "rows_per_launch": M},
         "roofline_train": {"kernels": "fwd_kernel (train) + bwd_kernel + wgrad_kernel + "
                                       "reduce_kernel", "bound": "hbm", "achieved": train_gbs,
