@@ -58,8 +58,10 @@ PackGeom pack_geom(const mlp* h) {
   const int W = h->width, L = n_mats(h);
   PackGeom g{};
   uint32_t total = 0;
+  // Every packed layer has kblocks(W) k-blocks (zero-padded past a smaller
+  // fan), so the kernels' contraction depth is a compile-time constant.
   for (int l = 0; l < L; ++l) {
-    const uint32_t f = (uint32_t)strips(fan_out_of(h, l)) * kblocks(fan_in_of(h, l));
+    const uint32_t f = (uint32_t)strips(fan_out_of(h, l)) * kblocks(W);
     if (l == 0) g.fwd_frag[0] = f;
     if (l == 1) g.fwd_frag[1] = f;
     total += f;
@@ -67,7 +69,7 @@ PackGeom pack_geom(const mlp* h) {
   g.fwd_total = total;
   g.fwd_frag[1] = (uint32_t)strips(W) * kblocks(W);
   uint32_t bt = 0;
-  for (int l = 1; l < L; ++l) bt += (uint32_t)strips(fan_in_of(h, l)) * kblocks(fan_out_of(h, l));
+  for (int l = 1; l < L; ++l) bt += (uint32_t)strips(fan_in_of(h, l)) * kblocks(W);
   g.bwd_hidden = (uint32_t)strips(W) * kblocks(W);
   g.bwd_total = bt;
   return g;
@@ -226,6 +228,49 @@ hipError_t device_info(DeviceInfo* out) {
     have[dev] = 1;
   }
   *out = cache[dev];
+  return hipSuccess;
+}
+
+hipError_t kernel_occupancy(const void* kernel, int threads, size_t lds, int* blocks_per_cu) {
+  struct Key {
+    int dev;
+    const void* k;
+    size_t lds;
+    int threads;
+  };
+  struct Limit {
+    int dev;
+    const void* k;
+    size_t lds;  // the largest dynamic-LDS limit set so far
+  };
+  static std::mutex mu;
+  static std::vector<std::pair<Key, int>> cache;
+  static std::vector<Limit> limits;
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  for (const auto& kv : cache)
+    if (kv.first.dev == dev && kv.first.k == kernel && kv.first.lds == lds &&
+        kv.first.threads == threads) {
+      *blocks_per_cu = kv.second;
+      return hipSuccess;
+    }
+  // The limit only ever grows, so configurations cached earlier stay valid.
+  Limit* lim = nullptr;
+  for (auto& x : limits)
+    if (x.dev == dev && x.k == kernel) lim = &x;
+  if (!lim || lim->lds < lds) {
+    e = hipFuncSetAttribute(kernel, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+    if (e != hipSuccess) return e;
+    if (lim) lim->lds = lds; else limits.push_back(Limit{dev, kernel, lds});
+  }
+  int occ = 0;
+  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kernel, threads, lds);
+  if (e != hipSuccess) return e;
+  if (occ < 1) occ = 1;
+  cache.push_back({Key{dev, kernel, lds, threads}, occ});
+  *blocks_per_cu = occ;
   return hipSuccess;
 }
 

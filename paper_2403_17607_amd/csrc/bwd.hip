@@ -28,7 +28,6 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
   const int64_t M = a.M;
   const int SO = (out_dim + 15) >> 4;
   const int OP = SO * 16;
-  const int KBO = (SO + 1) >> 1;
   const bool yvec = (out_dim & 3) == 0;
 
   if (a.resident && L > 1) {
@@ -107,14 +106,13 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
     // layer l-1 in chain order; it is also stored for the gradient kernel.
     // The derivative source of strip s is requested PF strips ahead.
     auto layer = [&](int l, const u32x4 (&in)[NT][KBW], u32x4 (&out)[NT][KBW]) {
-      const int KB = (l == L - 1) ? KBO : KBW;
       const uint32_t off = (uint32_t)(l - 1) * a.layH_frags;
       const u32x4* wl;
       if (a.resident) {
         wl = smem + (size_t)off * 64;
       } else {
         __syncthreads();
-        copy_frags(smem, a.packed + (size_t)off * 64, (uint32_t)(SW * KB), tid, NTH);
+        copy_frags(smem, a.packed + (size_t)off * 64, (uint32_t)(SW * KBW), tid, NTH);
         __syncthreads();
         wl = smem;
       }
@@ -141,20 +139,18 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
       static_for<0, SW>([&](auto sc) {
         constexpr int s = decltype(sc)::value;
         if constexpr (s + PF < SW) request(s + PF);
+        // every packed layer has KBW k-blocks (the output layer's are
+        // zero-padded past out_dim)
         u32x4 af[KBW];
 #pragma unroll
-        for (int kb = 0; kb < KBW; ++kb)
-          af[kb] = (kb < KB) ? wl[(s * KB + kb) * 64 + lane] : u32x4{0u, 0u, 0u, 0u};
+        for (int kb = 0; kb < KBW; ++kb) af[kb] = wl[(s * KBW + kb) * 64 + lane];
         f32x4 acc[NT];
 #pragma unroll
         for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) {
-          if (kb < KB) {
+        for (int kb = 0; kb < KBW; ++kb)
 #pragma unroll
-            for (int n = 0; n < NT; ++n) acc[n] = mfma16(af[kb], in[n][kb], acc[n]);
-          }
-        }
+          for (int n = 0; n < NT; ++n) acc[n] = mfma16(af[kb], in[n][kb], acc[n]);
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
           uint32_t p0, p1;
@@ -207,13 +203,9 @@ static hipError_t launch_t(const BwdArgs& a0, hipStream_t stream) {
   size_t lds = a.resident ? res_bytes : (size_t)a.layH_frags * 1024;
   if (lds == 0) lds = 16;
   auto kern = bwd_kernel<W, ACT, SEEDED>;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
   int occ = 0;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, NTH, lds);
+  e = kernel_occupancy(reinterpret_cast<const void*>(kern), NTH, lds, &occ);
   if (e != hipSuccess) return e;
-  if (occ < 1) occ = 1;
   int grid = di.cus * occ;
   if (grid > a.ntiles) grid = a.ntiles;
   if (grid < 1) grid = 1;

@@ -26,7 +26,8 @@
 //  * Packed weights (1 KiB fragments, [strip][k-block][lane][slot] bf16):
 //    forward layer l: A[j][p] = W_l[f(p)][j], j = output feature;
 //    backward layer l >= 1: A[f][p] = W_l[f][j(p)], f = input feature, for
-//    the delta product D_l^T = W_l D_{l+1}^T.  Out-of-range entries are 0.
+//    the delta product D_l^T = W_l D_{l+1}^T.  Every layer has the width's
+//    k-block count; out-of-range entries are 0.
 //
 //  * Tile image (stash tensors [M16][F], F a multiple of 16): the fp32 or
 //    bf16 result registers of a wave, stored as they are.  Element (m, f)
@@ -51,8 +52,8 @@ enum { ACT_LINEAR = 0, ACT_RELU = 1, ACT_SIGMOID = 2, ACT_SINE = 3 };
 // Rows per workgroup tile in the fused forward and backward kernels:
 // NT 16-row blocks per wave, NW waves per workgroup.
 template <int W> struct TileCfg;
-template <> struct TileCfg<16> { static constexpr int NT = 8, NW = 4; };
-template <> struct TileCfg<32> { static constexpr int NT = 8, NW = 4; };
+template <> struct TileCfg<16> { static constexpr int NT = 4, NW = 4; };
+template <> struct TileCfg<32> { static constexpr int NT = 4, NW = 4; };
 template <> struct TileCfg<64> { static constexpr int NT = 4, NW = 4; };
 template <> struct TileCfg<128> { static constexpr int NT = 4, NW = 8; };
 
@@ -170,5 +171,11 @@ struct DeviceInfo {
   int max_lds;  // bytes of LDS one workgroup may use
 };
 hipError_t device_info(DeviceInfo* out);
+
+// Prepares `kernel` on the current device for `lds` bytes of dynamic LDS
+// (raising its limit when needed) and returns how many of its workgroups
+// of `threads` fit on one compute unit.  Cached per (device, kernel, lds),
+// so repeated launches make no runtime queries.
+hipError_t kernel_occupancy(const void* kernel, int threads, size_t lds, int* blocks_per_cu);
 
 }  // namespace ffmlp

@@ -19,27 +19,24 @@
 
 namespace ffmlp {
 
+// Weight fragments of strip s.  Every packed layer has KBW k-blocks (the
+// first layer's are zero-padded past in_dim), so the count is a constant.
 template <int KBW>
-__device__ __forceinline__ void load_frags(const u32x4* wl, int s, int KB, int lane,
-                                           u32x4 (&af)[KBW]) {
+__device__ __forceinline__ void load_frags(const u32x4* wl, int s, int lane, u32x4 (&af)[KBW]) {
 #pragma unroll
-  for (int kb = 0; kb < KBW; ++kb)
-    af[kb] = (kb < KB) ? wl[(s * KB + kb) * 64 + lane] : u32x4{0u, 0u, 0u, 0u};
+  for (int kb = 0; kb < KBW; ++kb) af[kb] = wl[(s * KBW + kb) * 64 + lane];
 }
 
-// acc[n] = (one 16-feature strip of the packed layer) x act[n], KB k-blocks.
+// acc[n] = (one 16-feature strip of the packed layer) x act[n].
 template <int NT, int KBW>
-__device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], int KB,
-                                              const u32x4 (&act)[NT][KBW], f32x4 (&acc)[NT]) {
+__device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], const u32x4 (&act)[NT][KBW],
+                                              f32x4 (&acc)[NT]) {
 #pragma unroll
   for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-  for (int kb = 0; kb < KBW; ++kb) {
-    if (kb < KB) {
+  for (int kb = 0; kb < KBW; ++kb)
 #pragma unroll
-      for (int n = 0; n < NT; ++n) acc[n] = mfma16(af[kb], act[n][kb], acc[n]);
-    }
-  }
+    for (int n = 0; n < NT; ++n) acc[n] = mfma16(af[kb], act[n][kb], acc[n]);
 }
 
 template <int W, int ACT, int MODE>
@@ -68,8 +65,55 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
     copy_frags(smem, a.packed, a.total_frags, tid, NTH);
     __syncthreads();
   }
+  // A_1 = X of a wave tile, in input order: lane group g takes features
+  // 32 kb + 8 g .. + 7.
+  auto load_x = [&](int tile, u32x4 (&dst)[NT][KBW]) {
+    const int64_t r0 = (((int64_t)tile * NW + wave) * NT) * 16;
+    int64_t vr = M - r0;
+    vr = vr < 0 ? 0 : (vr > NT * 16 ? NT * 16 : vr);
+    if (xvec) {
+      // per-lane byte offset inside a 16-row block; the block goes in the
+      // scalar offset
+      const rsrc_t xr = make_rsrc(a.X + r0 * in_dim, vr * in_dim * 2);
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb) {
+        const int f0 = kb * 32 + lg * 8;
+        const uint32_t voff = (kb < KB0 && f0 < in_dim) ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
+#pragma unroll
+        for (int n = 0; n < NT; ++n) dst[n][kb] = bload128(xr, voff, (uint32_t)(n * 32 * in_dim));
+      }
+    } else {
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const int64_t m = r0 + n * 16 + li;
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+          const int f0 = kb * 32 + lg * 8;
+          uint32_t e[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+          if (kb < KB0 && m < M && f0 < in_dim) {
+            const uint16_t* xp = a.X + m * in_dim + f0;
+#pragma unroll
+            for (int q = 0; q < 8; ++q) e[q] = (f0 + q < in_dim) ? (uint32_t)xp[q] : 0u;
+          }
+          dst[n][kb] = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
+                             e[6] | (e[7] << 16)};
+        }
+      }
+    }
+  };
+  // Narrow nets have registers to spare for the X of later tiles: each
+  // wave requests X two tiles ahead (two buffers, used in turn by a tile
+  // loop unrolled by two).  Wider nets load X at the start of each tile.
+  constexpr bool XPF = W <= 32;
+  u32x4 xq0[XPF ? NT : 1][KBW], xq1[XPF ? NT : 1][KBW];
+  const int G = gridDim.x;
+  if constexpr (XPF) {
+    if ((int)blockIdx.x < a.ntiles) load_x(blockIdx.x, xq0);
+    if ((int)blockIdx.x + G < a.ntiles) load_x(blockIdx.x + G, xq1);
+  }
+
   float loss = 0.f;
-  for (int tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+  auto tile_body = [&](int tile, u32x4 (&xq)[XPF ? NT : 1][KBW]) {
     const int64_t tb0 = ((int64_t)tile * NW + wave) * NT;  // first 16-row block
     const int64_t row0 = tb0 * 16;
     int64_t vrows = M - row0;  // valid rows of this wave's tile
@@ -80,37 +124,15 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
     // (hidden layers go in pairs), so no register array is ever copied.
     u32x4 actA[NT][KBW], actB[NT][KBW];
     u32x4 afb[2][KBW];
-    if (resident && L > 1) load_frags<KBW>(smem, 0, KB0, lane, afb[0]);
-
-    // A_1 = X in input order: lane group g takes features 32 kb + 8 g .. + 7.
-    if (xvec) {
-      // per-lane byte offset inside a 16-row block; the block goes in the
-      // scalar offset
-      const rsrc_t xr = make_rsrc(a.X + row0 * in_dim, vrows * in_dim * 2);
+    if (resident && L > 1) load_frags<KBW>(smem, 0, lane, afb[0]);
+    if constexpr (XPF) {
 #pragma unroll
-      for (int kb = 0; kb < KBW; ++kb) {
-        const int f0 = kb * 32 + lg * 8;
-        const uint32_t voff = (kb < KB0 && f0 < in_dim) ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
+      for (int n = 0; n < NT; ++n)
 #pragma unroll
-        for (int n = 0; n < NT; ++n) actA[n][kb] = bload128(xr, voff, (uint32_t)(n * 32 * in_dim));
-      }
+        for (int kb = 0; kb < KBW; ++kb) actA[n][kb] = xq[n][kb];
+      if (tile + 2 * G < a.ntiles) load_x(tile + 2 * G, xq);
     } else {
-#pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        const int64_t m = row0 + n * 16 + li;
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) {
-          const int f0 = kb * 32 + lg * 8;
-          uint32_t e[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
-          if (kb < KB0 && m < M && f0 < in_dim) {
-            const uint16_t* xr = a.X + m * in_dim + f0;
-#pragma unroll
-            for (int q = 0; q < 8; ++q) e[q] = (f0 + q < in_dim) ? (uint32_t)xr[q] : 0u;
-          }
-          actA[n][kb] = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
-                              e[6] | (e[7] << 16)};
-        }
-      }
+      load_x(tile, actA);
     }
 
     // Hidden layer l: out = bf16(sigma(in W_l)) in the next layer's chain
@@ -118,16 +140,15 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
     // fragment buffer of strip s is (P * SW + s) % 2.
     auto hidden = [&](auto Pc, int l, const u32x4 (&in)[NT][KBW], u32x4 (&out)[NT][KBW]) {
       constexpr int P = decltype(Pc)::value;
-      const int KB = (l == 0) ? KB0 : KBW;
       const u32x4* wl;
       if (resident) {
         wl = smem + (size_t)layer_off(l) * 64;
       } else {
         __syncthreads();
-        copy_frags(smem, a.packed + (size_t)layer_off(l) * 64, (uint32_t)(SW * KB), tid, NTH);
+        copy_frags(smem, a.packed + (size_t)layer_off(l) * 64, (uint32_t)(SW * KBW), tid, NTH);
         __syncthreads();
         wl = smem;
-        load_frags<KBW>(wl, 0, KB, lane, afb[(P * SW) & 1]);
+        load_frags<KBW>(wl, 0, lane, afb[(P * SW) & 1]);
       }
       const size_t soff = (size_t)l * a.M16 * W + (size_t)row0 * W;
       const rsrc_t sa = make_rsrc(a.stashA + soff, a.stashA ? (int64_t)vblk * 32 * W : 0);
@@ -144,13 +165,13 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
         constexpr int s = decltype(sc)::value;
         constexpr int cur = (P * SW + s) & 1;
         if constexpr (s + 1 < SW) {
-          load_frags<KBW>(wl, s + 1, KB, lane, afb[cur ^ 1]);
+          load_frags<KBW>(wl, s + 1, lane, afb[cur ^ 1]);
         } else {
           if (resident && l + 1 < L - 1)
-            load_frags<KBW>(smem + (size_t)layer_off(l + 1) * 64, 0, KBW, lane, afb[cur ^ 1]);
+            load_frags<KBW>(smem + (size_t)layer_off(l + 1) * 64, 0, lane, afb[cur ^ 1]);
         }
         f32x4 acc[NT];
-        strip_product<NT, KBW>(afb[cur], KB, in, acc);
+        strip_product<NT, KBW>(afb[cur], in, acc);
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
           uint32_t p0, p1;
@@ -187,13 +208,12 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
     // output delta 2 (Y - T) / (M out_dim) * sigma_out'(C_L).
     auto output = [&](const u32x4 (&in)[NT][KBW]) {
       const int l = L - 1;
-      const int KB = (l == 0) ? KB0 : KBW;
       const u32x4* wl;
       if (resident) {
         wl = smem + (size_t)layer_off(l) * 64;
       } else {
         __syncthreads();
-        copy_frags(smem, a.packed + (size_t)layer_off(l) * 64, (uint32_t)(SO * KB), tid, NTH);
+        copy_frags(smem, a.packed + (size_t)layer_off(l) * 64, (uint32_t)(SO * KBW), tid, NTH);
         __syncthreads();
         wl = smem;
       }
@@ -203,9 +223,9 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       const rsrc_t cr = make_rsrc(a.cOut + row0 * OP, a.cOut ? (int64_t)vblk * 64 * OP : 0);
       for (int s = 0; s < SO; ++s) {
         u32x4 af[KBW];
-        load_frags<KBW>(wl, s, KB, lane, af);
+        load_frags<KBW>(wl, s, lane, af);
         f32x4 acc[NT];
-        strip_product<NT, KBW>(af, KB, in, acc);
+        strip_product<NT, KBW>(af, in, acc);
         const int j0 = s * 16 + lg * 4;
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
@@ -275,6 +295,15 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
     } else {
       output(actA);
     }
+  };
+
+  if constexpr (XPF) {
+    for (int tile = blockIdx.x; tile < a.ntiles; tile += 2 * G) {
+      tile_body(tile, xq0);
+      if (tile + G < a.ntiles) tile_body(tile + G, xq1);
+    }
+  } else {
+    for (int tile = blockIdx.x; tile < a.ntiles; tile += G) tile_body(tile, xq0);
   }
 
   if constexpr (MODE == FWD_TRAIN) {
@@ -298,24 +327,15 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
   hipError_t e = device_info(&di);
   if (e != hipSuccess) return e;
   const int KBW = (W + 31) / 32, SW = W / 16;
-  const int KB0 = (a.in_dim + 31) / 32, SO = (a.out_dim + 15) / 16;
-  uint32_t maxf = a.lay0_frags;
-  if (a.L > 1) {
-    maxf = maxf > (uint32_t)(SW * KBW) ? maxf : (uint32_t)(SW * KBW);
-  } else {
-    maxf = (uint32_t)(SO * KB0);
-  }
+  const int SO = (a.out_dim + 15) / 16;
+  const uint32_t maxf = (uint32_t)((a.L > 1 ? SW : SO) * KBW);
   const size_t res_bytes = (size_t)a.total_frags * 1024;
   a.resident = res_bytes + 1024 <= (size_t)di.max_lds ? 1 : 0;
   const size_t lds = a.resident ? res_bytes : (size_t)maxf * 1024;
   auto kern = fwd_kernel<W, ACT, MODE>;
-  e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                          hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
-  if (e != hipSuccess) return e;
   int occ = 0;
-  e = hipOccupancyMaxActiveBlocksPerMultiprocessor(&occ, kern, NTH, lds);
+  e = kernel_occupancy(reinterpret_cast<const void*>(kern), NTH, lds, &occ);
   if (e != hipSuccess) return e;
-  if (occ < 1) occ = 1;
   int grid = di.cus * occ;
   if (grid > a.ntiles) grid = a.ntiles;
   if (grid > kMaxLossParts) grid = kMaxLossParts;

@@ -313,15 +313,15 @@ __global__ __launch_bounds__(256) void pack_kernel(const PackArgs a) {
     if (l == L) { dir = 1; l = 1; woff = (int64_t)fan_in(0) * fan_out(0); }
     if (l >= L) return;  // not reached: e0 < total
     const int fi = fan_in(l), fo = fan_out(l);
-    const int rows = dir == 0 ? fo : fi, cols = dir == 0 ? fi : fo;
-    const int64_t n = (int64_t)((rows + 15) / 16) * ((cols + 31) / 32) * 512;
+    const int rows = dir == 0 ? fo : fi;
+    const int64_t n = (int64_t)((rows + 15) / 16) * ((Wd + 31) / 32) * 512;
     if (e < n) break;
     e -= n;
     woff += (int64_t)fi * fo;
     if (dir == 1 && l == L - 1) return;
   }
   const int fi = fan_in(l), fo = fan_out(l);
-  const int kblocks = dir == 0 ? (fi + 31) / 32 : (fo + 31) / 32;
+  const int kblocks = (Wd + 31) / 32;  // every layer is padded to the width's k-blocks
   const int slot = (int)(e & 7), lane = (int)((e >> 3) & 63);
   const int frag = (int)(e >> 9);
   const int s = frag / kblocks, kb = frag - s * kblocks;
@@ -348,8 +348,8 @@ static hipError_t wgrad_t(const WgradArgs& a, hipStream_t stream) {
     if (red > lds) lds = red;
   }
   auto kern = wgrad_kernel<W>;
-  hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(kern),
-                                     hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  int occ = 0;
+  hipError_t e = kernel_occupancy(reinterpret_cast<const void*>(kern), 256, lds, &occ);
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(kern, dim3(a.P, a.L), dim3(256), lds, stream, a);
   return hipGetLastError();

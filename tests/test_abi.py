@@ -49,12 +49,12 @@ def test_shapes_and_offsets(ffmlp, width):
     assert offs == [0, in_dim * width, in_dim * width + width * width,
                     in_dim * width + 2 * width * width]
     assert net.param_count() == offs[-1] + width * out_dim
-    # packed: forward strips(fan_out) x kblocks(fan_in) + backward layers
-    # 1..L-1 strips(fan_in) x kblocks(fan_out), 1 KiB per fragment.
+    # packed: forward strips(fan_out) + backward layers 1..L-1 strips(fan_in),
+    # each with the width's k-blocks, 1 KiB per fragment.
     st = lambda n: (n + 15) // 16
-    kb = lambda n: (n + 31) // 32
-    fwd = sum(st(fo) * kb(fi) for fi, fo, _ in shapes)
-    bwd = sum(st(fi) * kb(fo) for fi, fo, _ in shapes[1:])
+    kb = (width + 31) // 32
+    fwd = sum(st(fo) * kb for fi, fo, _ in shapes)
+    bwd = sum(st(fi) * kb for fi, fo, _ in shapes[1:])
     assert net.packed_bytes() == (fwd + bwd) * 1024
 
 
