@@ -30,9 +30,25 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
   const int OP = SO * 16;
   const bool yvec = (out_dim & 3) == 0;
 
-  if (a.resident && L > 1) {
-    copy_frags(smem, a.packed, a.total_frags, tid, NTH);
-    __syncthreads();
+  // Weights: resident in LDS, or staged layer by layer through two LDS
+  // buffers with direct-to-LDS loads, the next layer (layer L-1 of the next
+  // tile after layer 1) loading while the current one computes.
+  const bool resident = a.resident != 0;
+  const uint32_t bufq = (uint32_t)(SW * KBW) * 64;  // one buffer, in u32x4
+  int step = 0;
+  auto stream_buf = [&](int st) { return smem + ((st & 1) ? bufq : 0u); };
+  auto stage_layer = [&](int l, int st) {
+    stage_frags(stream_buf(st), a.packed + (size_t)(l - 1) * a.layH_frags * 64,
+                (uint32_t)(SW * KBW), wave, NW, lane);
+  };
+  if (L > 1) {
+    if (resident) {
+      copy_frags(smem, a.packed, a.total_frags, tid, NTH);
+      __syncthreads();
+    } else if ((int)blockIdx.x < a.ntiles) {
+      stage_layer(L - 1, 0);
+      drain_and_sync();
+    }
   }
   for (int tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
     const int64_t tb0 = ((int64_t)tile * NW + wave) * NT;
@@ -106,15 +122,13 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
     // layer l-1 in chain order; it is also stored for the gradient kernel.
     // The derivative source of strip s is requested PF strips ahead.
     auto layer = [&](int l, const u32x4 (&in)[NT][KBW], u32x4 (&out)[NT][KBW]) {
-      const uint32_t off = (uint32_t)(l - 1) * a.layH_frags;
       const u32x4* wl;
-      if (a.resident) {
-        wl = smem + (size_t)off * 64;
+      if (resident) {
+        wl = smem + (size_t)(l - 1) * a.layH_frags * 64;
       } else {
-        __syncthreads();
-        copy_frags(smem, a.packed + (size_t)off * 64, (uint32_t)(SW * KBW), tid, NTH);
-        __syncthreads();
-        wl = smem;
+        wl = stream_buf(step);
+        if (l - 1 >= 1) stage_layer(l - 1, step + 1);
+        else if (tile + (int)gridDim.x < a.ntiles) stage_layer(L - 1, step + 1);
       }
       const size_t toff = (size_t)(l - 1) * a.M16 * W + (size_t)row0 * W;
       const rsrc_t gsrc = make_rsrc((ACT == ACT_SINE ? a.stashS : a.stashA) + toff, (int64_t)vblk * 32 * W);
@@ -179,6 +193,10 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
         // Keep each strip's work together: bounds the live registers.
         __builtin_amdgcn_sched_barrier(0);
       });
+      if (!resident) {
+        drain_and_sync();  // next layer staged; this buffer free again
+        ++step;
+      }
     };
 
     // Layers in pairs with two delta buffers, so no register array is copied.
@@ -200,7 +218,7 @@ static hipError_t launch_t(const BwdArgs& a0, hipStream_t stream) {
   if (e != hipSuccess) return e;
   const size_t res_bytes = (size_t)a.total_frags * 1024;
   a.resident = res_bytes + 1024 <= (size_t)di.max_lds ? 1 : 0;
-  size_t lds = a.resident ? res_bytes : (size_t)a.layH_frags * 1024;
+  size_t lds = a.resident ? res_bytes : (size_t)2 * a.layH_frags * 1024;
   if (lds == 0) lds = 16;
   auto kern = bwd_kernel<W, ACT, SEEDED>;
   int occ = 0;

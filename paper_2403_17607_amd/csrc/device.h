@@ -125,6 +125,25 @@ __device__ __forceinline__ void copy_frags(u32x4* dst, const u32x4* src,
   for (uint32_t i = tid; i < n; i += nthreads) dst[i] = src[i];
 }
 
+// Asynchronous copy of nfrag 1 KiB fragments from global memory into LDS
+// with direct-to-LDS loads (no registers): wave w copies fragments w,
+// w + nwaves, ...; lane l of a load writes bytes 16 l .. 16 l + 15 of the
+// fragment.  The data is in LDS once the issuing wave has waited for its
+// vector memory counter; other waves may read it after a barrier.
+__device__ __forceinline__ void stage_frags(u32x4* dst, const u32x4* src, uint32_t nfrag,
+                                            int wave, int nwaves, int lane) {
+  for (uint32_t f = wave; f < nfrag; f += nwaves)
+    __builtin_amdgcn_global_load_lds((const void __attribute__((address_space(1)))*)(src + (size_t)f * 64 + lane),
+                                     (void __attribute__((address_space(3)))*)(dst + (size_t)f * 64), 16, 0, 0);
+}
+
+// Wait for every vector memory operation of this wave (direct-to-LDS loads
+// included), then synchronize the workgroup.
+__device__ __forceinline__ void drain_and_sync() {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+}
+
 // Deterministic wave-wide sum (fixed butterfly order).
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll

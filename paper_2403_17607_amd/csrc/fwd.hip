@@ -61,10 +61,31 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
     return l == 0 ? 0u : a.lay0_frags + (uint32_t)(l - 1) * a.layH_frags;
   };
 
+  // Weights: all layers resident in LDS, or (too large) layers staged in
+  // turn through two LDS buffers: while layer l computes from one buffer,
+  // the next layer (the first layer of the next tile after the last one)
+  // is loaded into the other with direct-to-LDS loads.  One barrier per
+  // layer.  `step` counts the layers this workgroup has run; its parity
+  // picks the buffer.
+  const uint32_t bufq = (uint32_t)((L > 1 ? SW : SO) * KBW) * 64;  // one buffer, in u32x4
+  int step = 0;
+  auto stream_buf = [&](int st) { return smem + ((st & 1) ? bufq : 0u); };
+  auto stage_layer = [&](int l, int st) {
+    const uint32_t nf = (uint32_t)((l == L - 1 ? SO : SW) * KBW);
+    stage_frags(stream_buf(st), a.packed + (size_t)layer_off(l) * 64, nf, wave, NW, lane);
+  };
   if (resident) {
     copy_frags(smem, a.packed, a.total_frags, tid, NTH);
     __syncthreads();
+  } else if ((int)blockIdx.x < a.ntiles) {
+    stage_layer(0, 0);
+    drain_and_sync();
   }
+  // Before layer l of `tile` runs (non-resident): request the next layer.
+  auto stage_next = [&](int l, int tile) {
+    if (l + 1 < L) stage_layer(l + 1, step + 1);
+    else if (tile + (int)gridDim.x < a.ntiles) stage_layer(0, step + 1);
+  };
   // A_1 = X of a wave tile, in input order: lane group g takes features
   // 32 kb + 8 g .. + 7.
   auto load_x = [&](int tile, u32x4 (&dst)[NT][KBW]) {
@@ -144,10 +165,8 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       if (resident) {
         wl = smem + (size_t)layer_off(l) * 64;
       } else {
-        __syncthreads();
-        copy_frags(smem, a.packed + (size_t)layer_off(l) * 64, (uint32_t)(SW * KBW), tid, NTH);
-        __syncthreads();
-        wl = smem;
+        wl = stream_buf(step);
+        stage_next(l, tile);
         load_frags<KBW>(wl, 0, lane, afb[(P * SW) & 1]);
       }
       const size_t soff = (size_t)l * a.M16 * W + (size_t)row0 * W;
@@ -202,6 +221,10 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
         // Keep each strip's work together: bounds the live registers.
         __builtin_amdgcn_sched_barrier(0);
       });
+      if (!resident) {
+        drain_and_sync();  // next layer staged; this buffer free again
+        ++step;
+      }
     };
 
     // Output layer: Y = sigma_out(C_L); when training also the loss and the
@@ -212,10 +235,8 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       if (resident) {
         wl = smem + (size_t)layer_off(l) * 64;
       } else {
-        __syncthreads();
-        copy_frags(smem, a.packed + (size_t)layer_off(l) * 64, (uint32_t)(SO * KBW), tid, NTH);
-        __syncthreads();
-        wl = smem;
+        wl = stream_buf(step);
+        stage_next(l, tile);
       }
       const rsrc_t yr = make_rsrc(a.Y + row0 * out_dim, a.Y ? vrows * out_dim * 2 : 0);
       const rsrc_t tr = make_rsrc(a.T + row0 * out_dim, a.T ? vrows * out_dim * 4 : 0);
@@ -282,6 +303,10 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
           }
         }
       }
+      if (!resident) {
+        drain_and_sync();
+        ++step;
+      }
     };
 
     int l = 0;
@@ -331,7 +356,7 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
   const uint32_t maxf = (uint32_t)((a.L > 1 ? SW : SO) * KBW);
   const size_t res_bytes = (size_t)a.total_frags * 1024;
   a.resident = res_bytes + 1024 <= (size_t)di.max_lds ? 1 : 0;
-  const size_t lds = a.resident ? res_bytes : (size_t)maxf * 1024;
+  const size_t lds = a.resident ? res_bytes : (size_t)2 * maxf * 1024;
   auto kern = fwd_kernel<W, ACT, MODE>;
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), NTH, lds, &occ);
