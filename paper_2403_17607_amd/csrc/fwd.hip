@@ -39,7 +39,10 @@ __device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], const u32x
     for (int n = 0; n < NT; ++n) acc[n] = mfma16(af[kb], act[n][kb], acc[n]);
 }
 
-template <int W, int ACT, int MODE>
+// FU selects the tile loop: 0 general; 1 and 2 the fused last layers (see
+// below) for L odd and L even, each its own kernel so that the register
+// allocation of one loop does not constrain the other.
+template <int W, int ACT, int MODE, int FU>
 __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs a) {
   constexpr int NT = TileCfg<W>::NT, NW = TileCfg<W>::NW, NTH = NW * 64;
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
@@ -74,12 +77,12 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
     const uint32_t nf = (uint32_t)((l == L - 1 ? SO : SW) * KBW);
     stage_frags(stream_buf(st), a.packed + (size_t)layer_off(l) * 64, nf, wave, NW, lane);
   };
+  // Weight loads are issued here and waited for after the first X loads
+  // below, so the two overlap.
   if (resident) {
-    copy_frags(smem, a.packed, a.total_frags, tid, NTH);
-    __syncthreads();
+    stage_frags(smem, a.packed, a.total_frags, wave, NW, lane);
   } else if ((int)blockIdx.x < a.ntiles) {
     stage_layer(0, 0);
-    drain_and_sync();
   }
   // Before layer l of `tile` runs (non-resident): request the next layer.
   auto stage_next = [&](int l, int tile) {
@@ -88,11 +91,12 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
   };
   // A_1 = X of a wave tile, in input order: lane group g takes features
   // 32 kb + 8 g .. + 7.
-  auto load_x = [&](int tile, u32x4 (&dst)[NT][KBW]) {
+  // With VEC (in_dim a multiple of 8) each lane reads 16-byte pieces.
+  auto load_x_t = [&](auto VECc, int tile, u32x4 (&dst)[NT][KBW]) {
     const int64_t r0 = (((int64_t)tile * NW + wave) * NT) * 16;
     int64_t vr = M - r0;
     vr = vr < 0 ? 0 : (vr > NT * 16 ? NT * 16 : vr);
-    if (xvec) {
+    if constexpr (decltype(VECc)::value) {
       // per-lane byte offset inside a 16-row block; the block goes in the
       // scalar offset
       const rsrc_t xr = make_rsrc(a.X + r0 * in_dim, vr * in_dim * 2);
@@ -122,19 +126,54 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       }
     }
   };
+  auto load_x = [&](int tile, u32x4 (&dst)[NT][KBW]) {
+    if (xvec) load_x_t(std::true_type{}, tile, dst);
+    else load_x_t(std::false_type{}, tile, dst);
+  };
+  auto load_xv = [&](int tile, u32x4 (&dst)[NT][KBW]) { load_x_t(std::true_type{}, tile, dst); };
   // Narrow nets have registers to spare for the X of later tiles: each
   // wave requests X two tiles ahead (two buffers, used in turn by a tile
-  // loop unrolled by two).  Wider nets load X at the start of each tile.
+  // loop unrolled by two).
   constexpr bool XPF = W <= 32;
+  // Wider inference nets whose layers are all resident and whose output is
+  // one 16-column strip run the last hidden layer and the output layer
+  // together: each k-block of A_{L-1} enters the output product as soon as
+  // its two strips exist, so A_{L-1} is never held whole and the second
+  // activation buffer is free during those two layers.  The next tile's X
+  // is requested into it there, hidden behind that work.
+  // The launcher picks FU != 0 only for inference with every layer
+  // resident, L >= 2, SO == 1 and in_dim a multiple of 8.
+  constexpr bool FUSE = FU != 0;
+  static_assert(!FUSE || (!XPF && MODE == FWD_INFER), "fused last layers: W >= 64, inference");
   u32x4 xq0[XPF ? NT : 1][KBW], xq1[XPF ? NT : 1][KBW];
+  u32x4 actA[NT][KBW], actB[NT][KBW];
   const int G = gridDim.x;
   if constexpr (XPF) {
     if ((int)blockIdx.x < a.ntiles) load_x(blockIdx.x, xq0);
     if ((int)blockIdx.x + G < a.ntiles) load_x(blockIdx.x + G, xq1);
+  } else if constexpr (FUSE) {
+    if ((int)blockIdx.x < a.ntiles) load_xv(blockIdx.x, actA);
   }
+  drain_and_sync();  // weights (the first layer, when streaming) in LDS
+
+  // bf16(sigma(c)) of one 16-row block's four features, as two bf16 pairs.
+  auto hid_act = [&](const f32x4& c, uint32_t& p0, uint32_t& p1) {
+    if constexpr (ACT == ACT_RELU) {
+      p0 = relu_bf16x2(pack_bf16x2(c[0], c[1]));
+      p1 = relu_bf16x2(pack_bf16x2(c[2], c[3]));
+    } else {
+      p0 = pack_bf16x2(act_hidden<ACT>(c[0]), act_hidden<ACT>(c[1]));
+      p1 = pack_bf16x2(act_hidden<ACT>(c[2]), act_hidden<ACT>(c[3]));
+    }
+  };
 
   float loss = 0.f;
-  auto tile_body = [&](int tile, u32x4 (&xq)[XPF ? NT : 1][KBW]) {
+  // One wave tile, with activation buffers bx (holding X) and by.  With F
+  // its X is already in bx (requested by the previous tile or before the
+  // loop); otherwise it comes from xq (XPF) or is loaded here.
+  auto tile_body = [&](int tile, u32x4 (&bx)[NT][KBW], u32x4 (&by)[NT][KBW], auto Fc,
+                       u32x4 (&xq)[XPF ? NT : 1][KBW]) {
+    constexpr bool F = decltype(Fc)::value;
     const int64_t tb0 = ((int64_t)tile * NW + wave) * NT;  // first 16-row block
     const int64_t row0 = tb0 * 16;
     int64_t vrows = M - row0;  // valid rows of this wave's tile
@@ -143,17 +182,16 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
 
     // Two activation buffers and two weight-fragment buffers, used in turn
     // (hidden layers go in pairs), so no register array is ever copied.
-    u32x4 actA[NT][KBW], actB[NT][KBW];
     u32x4 afb[2][KBW];
     if (resident && L > 1) load_frags<KBW>(smem, 0, lane, afb[0]);
     if constexpr (XPF) {
 #pragma unroll
       for (int n = 0; n < NT; ++n)
 #pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) actA[n][kb] = xq[n][kb];
+        for (int kb = 0; kb < KBW; ++kb) bx[n][kb] = xq[n][kb];
       if (tile + 2 * G < a.ntiles) load_x(tile + 2 * G, xq);
-    } else {
-      load_x(tile, actA);
+    } else if constexpr (!F) {
+      load_x(tile, bx);
     }
 
     // Hidden layer l: out = bf16(sigma(in W_l)) in the next layer's chain
@@ -194,13 +232,7 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
           uint32_t p0, p1;
-          if constexpr (ACT == ACT_RELU) {
-            p0 = relu_bf16x2(pack_bf16x2(acc[n][0], acc[n][1]));
-            p1 = relu_bf16x2(pack_bf16x2(acc[n][2], acc[n][3]));
-          } else {
-            p0 = pack_bf16x2(act_hidden<ACT>(acc[n][0]), act_hidden<ACT>(acc[n][1]));
-            p1 = pack_bf16x2(act_hidden<ACT>(acc[n][2]), act_hidden<ACT>(acc[n][3]));
-          }
+          hid_act(acc[n], p0, p1);
           if constexpr (s & 1) {
             out[n][s >> 1].z = p0;
             out[n][s >> 1].w = p1;
@@ -227,8 +259,72 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       }
     };
 
-    // Output layer: Y = sigma_out(C_L); when training also the loss and the
-    // output delta 2 (Y - T) / (M out_dim) * sigma_out'(C_L).
+    // Everything after the product of output strip s: Y = sigma_out(C_L);
+    // when training also the loss and the output delta
+    // 2 (Y - T) / (M out_dim) * sigma_out'(C_L); when stashing C_L.
+    auto out_strip = [&](int s, const f32x4 (&acc)[NT]) {
+      const rsrc_t yr = make_rsrc(a.Y + row0 * out_dim, a.Y ? vrows * out_dim * 2 : 0);
+      const int j0 = s * 16 + lg * 4;
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const int64_t m = row0 + n * 16 + li;
+        const bool ok = (m < M) && (j0 < out_dim);
+        // element offset of (row li, j0) inside the block (past the end if
+        // the column is); the block's offset goes in the scalar offset
+        const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
+        const uint32_t bo = (uint32_t)(n * 16 * out_dim);
+        float y[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) y[r] = act_apply(out_act, acc[n][r]);
+        const uint32_t y0 = pack_bf16x2(y[0], y[1]), y1 = pack_bf16x2(y[2], y[3]);
+        if (a.Y != nullptr) {
+          if (yvec) {
+            bstore64(u32x2{y0, y1}, yr, eo * 2, bo * 2);
+          } else if (ok) {
+            uint16_t* yp = a.Y + m * out_dim + j0;
+            const uint16_t yb[4] = {(uint16_t)(y0 & 0xffff), (uint16_t)(y0 >> 16),
+                                    (uint16_t)(y1 & 0xffff), (uint16_t)(y1 >> 16)};
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (j0 + r < out_dim) yp[r] = yb[r];
+          }
+        }
+        if constexpr (MODE == FWD_TRAIN) {
+          const rsrc_t tr = make_rsrc(a.T + row0 * out_dim, a.T ? vrows * out_dim * 4 : 0);
+          const rsrc_t dr = make_rsrc(a.deltaOut + row0 * OP, a.deltaOut ? (int64_t)vblk * 32 * OP : 0);
+          float t[4] = {0.f, 0.f, 0.f, 0.f};
+          if (yvec) {
+            const u32x4 tv = bload128(tr, eo * 4, bo * 4);
+            t[0] = __uint_as_float(tv.x);
+            t[1] = __uint_as_float(tv.y);
+            t[2] = __uint_as_float(tv.z);
+            t[3] = __uint_as_float(tv.w);
+          } else if (ok) {
+            const float* tp = a.T + m * out_dim + j0;
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (j0 + r < out_dim) t[r] = tp[r];
+          }
+          float d[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            const bool valid = ok && (j0 + r < out_dim);
+            const float diff = y[r] - t[r];
+            if (valid) loss += diff * diff;
+            d[r] = valid ? (a.scale * diff) * act_out_grad(out_act, acc[n][r], y[r]) : 0.f;
+          }
+          bstore64(u32x2{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])}, dr, lane * 8,
+                   (uint32_t)((n * SO + s) * 512));
+        }
+        if constexpr (MODE == FWD_STASH) {
+          const rsrc_t cr = make_rsrc(a.cOut + row0 * OP, a.cOut ? (int64_t)vblk * 64 * OP : 0);
+          bstore128(__builtin_bit_cast(u32x4, acc[n]), cr, lane * 16,
+                    (uint32_t)((n * SO + s) * 1024));
+        }
+      }
+    };
+
+    // Output layer on its own.
     auto output = [&](const u32x4 (&in)[NT][KBW]) {
       const int l = L - 1;
       const u32x4* wl;
@@ -238,70 +334,12 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
         wl = stream_buf(step);
         stage_next(l, tile);
       }
-      const rsrc_t yr = make_rsrc(a.Y + row0 * out_dim, a.Y ? vrows * out_dim * 2 : 0);
-      const rsrc_t tr = make_rsrc(a.T + row0 * out_dim, a.T ? vrows * out_dim * 4 : 0);
-      const rsrc_t dr = make_rsrc(a.deltaOut + row0 * OP, a.deltaOut ? (int64_t)vblk * 32 * OP : 0);
-      const rsrc_t cr = make_rsrc(a.cOut + row0 * OP, a.cOut ? (int64_t)vblk * 64 * OP : 0);
       for (int s = 0; s < SO; ++s) {
         u32x4 af[KBW];
         load_frags<KBW>(wl, s, lane, af);
         f32x4 acc[NT];
         strip_product<NT, KBW>(af, in, acc);
-        const int j0 = s * 16 + lg * 4;
-#pragma unroll
-        for (int n = 0; n < NT; ++n) {
-          const int64_t m = row0 + n * 16 + li;
-          const bool ok = (m < M) && (j0 < out_dim);
-          // element offset of (row li, j0) inside the block (past the end if
-          // the column is); the block's offset goes in the scalar offset
-          const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
-          const uint32_t bo = (uint32_t)(n * 16 * out_dim);
-          float y[4];
-#pragma unroll
-          for (int r = 0; r < 4; ++r) y[r] = act_apply(out_act, acc[n][r]);
-          const uint32_t y0 = pack_bf16x2(y[0], y[1]), y1 = pack_bf16x2(y[2], y[3]);
-          if (a.Y != nullptr) {
-            if (yvec) {
-              bstore64(u32x2{y0, y1}, yr, eo * 2, bo * 2);
-            } else if (ok) {
-              uint16_t* yp = a.Y + m * out_dim + j0;
-              const uint16_t yb[4] = {(uint16_t)(y0 & 0xffff), (uint16_t)(y0 >> 16),
-                                      (uint16_t)(y1 & 0xffff), (uint16_t)(y1 >> 16)};
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                if (j0 + r < out_dim) yp[r] = yb[r];
-            }
-          }
-          if constexpr (MODE == FWD_TRAIN) {
-            float t[4] = {0.f, 0.f, 0.f, 0.f};
-            if (yvec) {
-              const u32x4 tv = bload128(tr, eo * 4, bo * 4);
-              t[0] = __uint_as_float(tv.x);
-              t[1] = __uint_as_float(tv.y);
-              t[2] = __uint_as_float(tv.z);
-              t[3] = __uint_as_float(tv.w);
-            } else if (ok) {
-              const float* tp = a.T + m * out_dim + j0;
-#pragma unroll
-              for (int r = 0; r < 4; ++r)
-                if (j0 + r < out_dim) t[r] = tp[r];
-            }
-            float d[4];
-#pragma unroll
-            for (int r = 0; r < 4; ++r) {
-              const bool valid = ok && (j0 + r < out_dim);
-              const float diff = y[r] - t[r];
-              if (valid) loss += diff * diff;
-              d[r] = valid ? (a.scale * diff) * act_out_grad(out_act, acc[n][r], y[r]) : 0.f;
-            }
-            bstore64(u32x2{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])}, dr, lane * 8,
-                     (uint32_t)((n * SO + s) * 512));
-          }
-          if constexpr (MODE == FWD_STASH) {
-            bstore128(__builtin_bit_cast(u32x4, acc[n]), cr, lane * 16,
-                      (uint32_t)((n * SO + s) * 1024));
-          }
-        }
+        out_strip(s, acc);
       }
       if (!resident) {
         drain_and_sync();
@@ -309,26 +347,98 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       }
     };
 
+    // Last hidden layer (L - 2) and the one-strip output layer together
+    // (F only; every layer resident, SW even).  `nx` is free throughout:
+    // the next tile's X goes there.
+    auto last = [&](const u32x4 (&in)[NT][KBW], u32x4 (&nx)[NT][KBW]) {
+      const u32x4* wl = smem + (size_t)layer_off(L - 2) * 64;
+      const u32x4* wo = smem + (size_t)layer_off(L - 1) * 64;
+      if (tile + G < a.ntiles) load_xv(tile + G, nx);
+      f32x4 yacc[NT];
+#pragma unroll
+      for (int n = 0; n < NT; ++n) yacc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+      u32x4 kblk[NT];  // one k-block of A_{L-1}: strips 2 kb and 2 kb + 1
+      u32x4 wof;       // the output layer's fragment for that k-block
+      static_for<0, SW>([&](auto sc) {
+        constexpr int s = decltype(sc)::value;
+        constexpr int cur = s & 1;
+        if constexpr (s + 1 < SW) load_frags<KBW>(wl, s + 1, lane, afb[cur ^ 1]);
+        if constexpr ((s & 1) == 0) wof = wo[(s >> 1) * 64 + lane];
+        f32x4 acc[NT];
+        strip_product<NT, KBW>(afb[cur], in, acc);
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+          uint32_t p0, p1;
+          hid_act(acc[n], p0, p1);
+          if constexpr (s & 1) {
+            kblk[n].z = p0;
+            kblk[n].w = p1;
+          } else {
+            kblk[n].x = p0;
+            kblk[n].y = p1;
+          }
+        }
+        // the same k-block order and MFMA shape as the output layer on its
+        // own, so Y is bitwise the same as the training forward's
+        if constexpr (s & 1) {
+#pragma unroll
+          for (int n = 0; n < NT; ++n) yacc[n] = mfma16(wof, kblk[n], yacc[n]);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      out_strip(0, yacc);
+    };
+
+    using I0 = std::integral_constant<int, 0>;
+    using I1 = std::integral_constant<int, 1>;
     int l = 0;
-    for (; l + 2 <= L - 1; l += 2) {
-      hidden(std::integral_constant<int, 0>{}, l, actA, actB);
-      hidden(std::integral_constant<int, 1>{}, l + 1, actB, actA);
-    }
-    if (l < L - 1) {
-      hidden(std::integral_constant<int, 0>{}, l, actA, actB);
-      output(actB);
+    if constexpr (F) {
+      static_assert(SW % 2 == 0, "fused last layers need an even strip count");
+      for (; l + 2 <= L - 2; l += 2) {
+        hidden(I0{}, l, bx, by);
+        hidden(I1{}, l + 1, by, bx);
+      }
+      if (l < L - 2) {
+        hidden(I0{}, l, bx, by);
+        last(by, bx);
+      } else {
+        last(bx, by);
+      }
     } else {
-      output(actA);
+      for (; l + 2 <= L - 1; l += 2) {
+        hidden(I0{}, l, bx, by);
+        hidden(I1{}, l + 1, by, bx);
+      }
+      if (l < L - 1) {
+        hidden(I0{}, l, bx, by);
+        output(by);
+      } else {
+        output(bx);
+      }
     }
   };
 
+  using NoF = std::integral_constant<bool, false>;
   if constexpr (XPF) {
     for (int tile = blockIdx.x; tile < a.ntiles; tile += 2 * G) {
-      tile_body(tile, xq0);
-      if (tile + G < a.ntiles) tile_body(tile + G, xq1);
+      tile_body(tile, actA, actB, NoF{}, xq0);
+      if (tile + G < a.ntiles) tile_body(tile + G, actA, actB, NoF{}, xq1);
     }
+  } else if constexpr (FU == 2) {
+    // The last layers read A_{L-1} from the buffer the hidden chain ends
+    // in and the next X goes to the other one; with L even that is actB
+    // after a tile that started in actA and the reverse, so the loop
+    // alternates.
+    using Fu = std::integral_constant<bool, true>;
+    for (int tile = blockIdx.x; tile < a.ntiles; tile += 2 * G) {
+      tile_body(tile, actA, actB, Fu{}, xq0);
+      if (tile + G < a.ntiles) tile_body(tile + G, actB, actA, Fu{}, xq0);
+    }
+  } else if constexpr (FU == 1) {
+    using Fu = std::integral_constant<bool, true>;
+    for (int tile = blockIdx.x; tile < a.ntiles; tile += G) tile_body(tile, actA, actB, Fu{}, xq0);
   } else {
-    for (int tile = blockIdx.x; tile < a.ntiles; tile += G) tile_body(tile, xq0);
+    for (int tile = blockIdx.x; tile < a.ntiles; tile += G) tile_body(tile, actA, actB, NoF{}, xq0);
   }
 
   if constexpr (MODE == FWD_TRAIN) {
@@ -357,7 +467,11 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
   const size_t res_bytes = (size_t)a.total_frags * 1024;
   a.resident = res_bytes + 1024 <= (size_t)di.max_lds ? 1 : 0;
   const size_t lds = a.resident ? res_bytes : (size_t)2 * maxf * 1024;
-  auto kern = fwd_kernel<W, ACT, MODE>;
+  void (*kern)(FwdArgs) = fwd_kernel<W, ACT, MODE, 0>;
+  if constexpr (MODE == FWD_INFER && W >= 64) {
+    if (a.resident && a.L >= 2 && SO == 1 && (a.in_dim % 8) == 0)
+      kern = (a.L & 1) ? fwd_kernel<W, ACT, MODE, 1> : fwd_kernel<W, ACT, MODE, 2>;
+  }
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), NTH, lds, &occ);
   if (e != hipSuccess) return e;

@@ -208,9 +208,12 @@ def sampled_rows(M, n, seed):
     (32, 4, 32, 16, 1 << 20),
     (16, 4, 16, 16, 1 << 22),         # width sweep at 2^22
     (128, 16, 128, 128, 1 << 20),     # depth/width stress: weights stream through LDS
+    (128, 3, 128, 16, (1 << 20) + 100),  # even matrix count, ragged tail
+    (64, 5, 64, 16, 1 << 20),         # even matrix count at width 64
 ])
 def test_full_size_sampled(ffmlp, gpu, width, depth, in_dim, out_dim, M):
-    """At benchmark sizes: Y on sampled rows against the oracle, and G from
+    """At benchmark sizes: Y on sampled rows against the oracle, inference Y
+    bitwise equal to the stashing forward's on every row, and G from
     mlp_backward with dY nonzero only on the sampled rows (G is a sum over
     rows, so the oracle needs only those rows)."""
     log(f"full-size w={width} d={depth} M={M}")
@@ -226,6 +229,9 @@ def test_full_size_sampled(ffmlp, gpu, width, depth, in_dim, out_dim, M):
     packed = net.pack(W.to(gpu))
     ws = net.workspace(M, gpu)
     Y = net.forward(packed, Xd, stash=ws)
+    # inference (its own kernel and tile loop) computes every row the same
+    Yi = net.forward(packed, Xd)
+    assert torch.equal(Yi, Y), "inference outputs differ from the stashing forward's"
     dYs = datagen.uniform(14, datagen.STREAM_AUX, (len(rows), out_dim))
     dY = torch.zeros(M, out_dim, dtype=torch.float32, device=gpu)
     dY[rows.to(gpu)] = dYs.to(gpu)
