@@ -25,6 +25,13 @@ __device__ __forceinline__ uint32_t pack_bf16x2(float a, float b) {
   return __builtin_bit_cast(uint32_t, r);
 }
 
+// Keep the computation of v at this point of the program: an empty asm
+// that claims to change v, so the compiler can neither sink the work that
+// produced v towards v's later uses nor drop it.  A layer's activations
+// are otherwise converted only at the end of the layer, which keeps every
+// strip's fp32 accumulators alive until then.
+__device__ __forceinline__ void pin(uint32_t& v) { asm volatile("" : "+v"(v)); }
+
 // ReLU of two packed bf16 values: a bf16 value is <= 0 exactly when its bit
 // pattern read as int16 is <= 0, so a packed int16 max with 0 is ReLU.  It
 // commutes with rounding (rounding keeps the sign), so ReLU may be applied

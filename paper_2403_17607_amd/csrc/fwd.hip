@@ -233,6 +233,8 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
         for (int n = 0; n < NT; ++n) {
           uint32_t p0, p1;
           hid_act(acc[n], p0, p1);
+          pin(p0);
+          pin(p1);
           if constexpr (s & 1) {
             out[n][s >> 1].z = p0;
             out[n][s >> 1].w = p1;
@@ -370,6 +372,8 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
         for (int n = 0; n < NT; ++n) {
           uint32_t p0, p1;
           hid_act(acc[n], p0, p1);
+          pin(p0);
+          pin(p1);
           if constexpr (s & 1) {
             kblk[n].z = p0;
             kblk[n].w = p1;
