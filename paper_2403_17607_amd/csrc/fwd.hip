@@ -39,10 +39,13 @@ __device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], const u32x
     for (int n = 0; n < NT; ++n) acc[n] = mfma16(af[kb], act[n][kb], acc[n]);
 }
 
+// RES: every layer's weights resident in LDS (else staged layer by layer).
 // FU selects the tile loop: 0 general; 1 and 2 the fused last layers (see
-// below) for L odd and L even, each its own kernel so that the register
-// allocation of one loop does not constrain the other.
-template <int W, int ACT, int MODE, int FU>
+// below) for L odd and L even.  Each combination is its own kernel, so that
+// the register allocation of one loop does not constrain another and no
+// loop carries the other's branches (whose joins force conservative waits
+// on LDS loads).
+template <int W, int ACT, int MODE, int FU, bool RES>
 __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs a) {
   constexpr int NT = TileCfg<W>::NT, NW = TileCfg<W>::NW, NTH = NW * 64;
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
@@ -59,7 +62,8 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
   const bool xvec = (in_dim & 7) == 0;
   const bool yvec = (out_dim & 3) == 0;
   const int out_act = a.out_act;
-  const bool resident = a.resident != 0;
+  constexpr bool resident = RES;
+  const int G = gridDim.x;
   auto layer_off = [&](int l) -> uint32_t {
     return l == 0 ? 0u : a.lay0_frags + (uint32_t)(l - 1) * a.layH_frags;
   };
@@ -87,7 +91,7 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
   // Before layer l of `tile` runs (non-resident): request the next layer.
   auto stage_next = [&](int l, int tile) {
     if (l + 1 < L) stage_layer(l + 1, step + 1);
-    else if (tile + (int)gridDim.x < a.ntiles) stage_layer(0, step + 1);
+    else if (tile + G < a.ntiles) stage_layer(0, step + 1);
   };
   // A_1 = X of a wave tile, in input order: lane group g takes features
   // 32 kb + 8 g .. + 7.
@@ -147,7 +151,6 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
   static_assert(!FUSE || (!XPF && MODE == FWD_INFER), "fused last layers: W >= 64, inference");
   u32x4 xq0[XPF ? NT : 1][KBW], xq1[XPF ? NT : 1][KBW];
   u32x4 actA[NT][KBW], actB[NT][KBW];
-  const int G = gridDim.x;
   if constexpr (XPF) {
     if ((int)blockIdx.x < a.ntiles) load_x(blockIdx.x, xq0);
     if ((int)blockIdx.x + G < a.ntiles) load_x(blockIdx.x + G, xq1);
@@ -471,10 +474,11 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
   const size_t res_bytes = (size_t)a.total_frags * 1024;
   a.resident = res_bytes + 1024 <= (size_t)di.max_lds ? 1 : 0;
   const size_t lds = a.resident ? res_bytes : (size_t)2 * maxf * 1024;
-  void (*kern)(FwdArgs) = fwd_kernel<W, ACT, MODE, 0>;
+  void (*kern)(FwdArgs) =
+      a.resident ? fwd_kernel<W, ACT, MODE, 0, true> : fwd_kernel<W, ACT, MODE, 0, false>;
   if constexpr (MODE == FWD_INFER && W >= 64) {
     if (a.resident && a.L >= 2 && SO == 1 && (a.in_dim % 8) == 0)
-      kern = (a.L & 1) ? fwd_kernel<W, ACT, MODE, 1> : fwd_kernel<W, ACT, MODE, 2>;
+      kern = (a.L & 1) ? fwd_kernel<W, ACT, MODE, 1, true> : fwd_kernel<W, ACT, MODE, 2, true>;
   }
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), NTH, lds, &occ);
