@@ -16,9 +16,12 @@
 
 namespace ffmlp {
 
-template <int W, int ACT, int SEEDED>
+// RES: every layer's weights resident in LDS (else staged layer by layer);
+// each mode is its own kernel, so the tile loop carries no residency
+// branches (whose joins force conservative waits on LDS loads).
+template <int W, int ACT, int SEEDED, bool RES>
 __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs a) {
-  constexpr int NT = TileCfg<W>::NT, NW = TileCfg<W>::NW, NTH = NW * 64;
+  constexpr int NT = TileCfg<W>::NT, NW = TileCfg<W>::NW;
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
   extern __shared__ u32x4 smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -33,7 +36,8 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
   // Weights: resident in LDS, or staged layer by layer through two LDS
   // buffers with direct-to-LDS loads, the next layer (layer L-1 of the next
   // tile after layer 1) loading while the current one computes.
-  const bool resident = a.resident != 0;
+  constexpr bool resident = RES;
+  const int G = gridDim.x;
   const uint32_t bufq = (uint32_t)(SW * KBW) * 64;  // one buffer, in u32x4
   int step = 0;
   auto stream_buf = [&](int st) { return smem + ((st & 1) ? bufq : 0u); };
@@ -43,14 +47,13 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
   };
   if (L > 1) {
     if (resident) {
-      copy_frags(smem, a.packed, a.total_frags, tid, NTH);
-      __syncthreads();
+      stage_frags(smem, a.packed, a.total_frags, wave, NW, lane);
     } else if ((int)blockIdx.x < a.ntiles) {
       stage_layer(L - 1, 0);
-      drain_and_sync();
     }
+    drain_and_sync();
   }
-  for (int tile = blockIdx.x; tile < a.ntiles; tile += gridDim.x) {
+  for (int tile = blockIdx.x; tile < a.ntiles; tile += G) {
     const int64_t tb0 = ((int64_t)tile * NW + wave) * NT;
     const int64_t row0 = tb0 * 16;
     int64_t vrows = M - row0;  // valid rows of this wave's tile
@@ -128,7 +131,7 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
       } else {
         wl = stream_buf(step);
         if (l - 1 >= 1) stage_layer(l - 1, step + 1);
-        else if (tile + (int)gridDim.x < a.ntiles) stage_layer(L - 1, step + 1);
+        else if (tile + G < a.ntiles) stage_layer(L - 1, step + 1);
       }
       const size_t toff = (size_t)(l - 1) * a.M16 * W + (size_t)row0 * W;
       const rsrc_t gsrc = make_rsrc((ACT == ACT_SINE ? a.stashS : a.stashA) + toff, (int64_t)vblk * 32 * W);
@@ -220,7 +223,7 @@ static hipError_t launch_t(const BwdArgs& a0, hipStream_t stream) {
   a.resident = res_bytes + 1024 <= (size_t)di.max_lds ? 1 : 0;
   size_t lds = a.resident ? res_bytes : (size_t)2 * a.layH_frags * 1024;
   if (lds == 0) lds = 16;
-  auto kern = bwd_kernel<W, ACT, SEEDED>;
+  auto kern = a.resident ? bwd_kernel<W, ACT, SEEDED, true> : bwd_kernel<W, ACT, SEEDED, false>;
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), NTH, lds, &occ);
   if (e != hipSuccess) return e;

@@ -125,13 +125,6 @@ __device__ __forceinline__ void bstore128(u32x4 v, rsrc_t r, uint32_t voff, uint
   __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, 0);
 }
 
-// Cooperative copy of nfrag 1 KiB fragments from global memory into LDS.
-__device__ __forceinline__ void copy_frags(u32x4* dst, const u32x4* src,
-                                           uint32_t nfrag, int tid, int nthreads) {
-  const uint32_t n = nfrag * 64u;
-  for (uint32_t i = tid; i < n; i += nthreads) dst[i] = src[i];
-}
-
 // Asynchronous copy of nfrag 1 KiB fragments from global memory into LDS
 // with direct-to-LDS loads (no registers): wave w copies fragments w,
 // w + nwaves, ...; lane l of a load writes bytes 16 l .. 16 l + 15 of the

@@ -47,7 +47,7 @@ __device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], const u32x
 // on LDS loads).
 template <int W, int ACT, int MODE, int FU, bool RES>
 __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs a) {
-  constexpr int NT = TileCfg<W>::NT, NW = TileCfg<W>::NW, NTH = NW * 64;
+  constexpr int NT = TileCfg<W>::NT, NW = TileCfg<W>::NW;
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
   extern __shared__ u32x4 smem[];
   __shared__ float red[NW];
