@@ -43,16 +43,20 @@ def flops_per_row(width, depth, in_dim, out_dim):
 
 def train_bytes_per_row(width, depth, in_dim, out_dim, act):
     """HBM bytes the three-kernel training step must move per row:
-    forward reads X, T and writes the activations and the output delta;
-    backward reads the output delta and the activations (or the stored
-    cos for sine) and writes the hidden deltas; the gradient kernel reads
-    X, the activations, the hidden deltas and the output delta."""
+    forward reads X, T and writes the activations, the output delta and
+    (ReLU) the activation masks; backward reads the output delta and the
+    derivative source of every hidden activation (ReLU: its mask, 16 B per
+    row; sigmoid: the activation; sine: the stored cos; linear: nothing)
+    and writes the hidden deltas; the gradient kernel reads X, the
+    activations, the hidden deltas and the output delta."""
     OP = (out_dim + 15) // 16 * 16
     hid = depth * width * 2
-    b = 2 * in_dim + 4 * out_dim + hid + 2 * OP           # forward (train)
+    mask = depth * 16 if act == "relu" else 0
+    deriv = {"relu": mask, "linear": 0}.get(act, hid)
+    b = 2 * in_dim + 4 * out_dim + hid + 2 * OP + mask    # forward (train)
     if act == "sine":
         b += hid                                          # cos stash write
-    b += 2 * OP + hid + hid                               # backward
+    b += 2 * OP + deriv + hid                             # backward
     b += 2 * in_dim + hid + hid + 2 * OP                  # weight gradients
     return b
 

@@ -78,7 +78,7 @@ PackGeom pack_geom(const mlp* h) {
 // Workspace layout for a batch of M rows (byte offsets, 256-byte aligned).
 struct WsLayout {
   int64_t M16;
-  size_t stashA, stashS, deltaH, deltaOut, cOut, partial, mid, lossPart, total;
+  size_t stashA, stashS, reluMask, deltaH, deltaOut, cOut, partial, mid, lossPart, total;
   int P, chunks_per_block;
 };
 
@@ -91,6 +91,8 @@ WsLayout ws_layout(const mlp* h, int64_t M) {
   size_t o = 0;
   w.stashA = o; o = round_up(o + hid, 256);
   w.stashS = o; o = round_up(o + (h->act == MLP_ACT_SINE ? hid : 0), 256);
+  // ReLU masks: one 32-bit word per lane of every 16-row block and layer
+  w.reluMask = o; o = round_up(o + (h->act == MLP_ACT_RELU ? (size_t)(L - 1) * (w.M16 / 16) * 256 : 0), 256);
   w.deltaH = o; o = round_up(o + hid, 256);
   w.deltaOut = o; o = round_up(o + (size_t)w.M16 * OP * 2, 256);
   w.cOut = o; o = round_up(o + (h->out_act != MLP_ACT_LINEAR ? (size_t)w.M16 * OP * 4 : 0), 256);
@@ -154,6 +156,7 @@ BwdArgs bwd_args(const mlp* h, const void* packed, const WsLayout& w, uint8_t* w
   b.deltaH = reinterpret_cast<uint16_t*>(ws + w.deltaH);
   b.deltaOut = reinterpret_cast<uint16_t*>(ws + w.deltaOut);
   b.cOut = h->out_act != MLP_ACT_LINEAR ? reinterpret_cast<const float*>(ws + w.cOut) : nullptr;
+  b.reluMask = h->act == MLP_ACT_RELU ? reinterpret_cast<const uint32_t*>(ws + w.reluMask) : nullptr;
   b.M = M;
   b.M16 = w.M16;
   b.out_dim = h->out_dim;
@@ -372,6 +375,7 @@ int mlp_forward(const mlp_t* h, const void* packed, const uint16_t* X, uint16_t*
     uint8_t* ws = static_cast<uint8_t*>(stash);
     a.stashA = reinterpret_cast<uint16_t*>(ws + w.stashA);
     a.stashS = h->act == MLP_ACT_SINE ? reinterpret_cast<uint16_t*>(ws + w.stashS) : nullptr;
+    a.reluMask = h->act == MLP_ACT_RELU ? reinterpret_cast<uint32_t*>(ws + w.reluMask) : nullptr;
     a.cOut = h->out_act != MLP_ACT_LINEAR ? reinterpret_cast<float*>(ws + w.cOut) : nullptr;
     mode = FWD_STASH;
   }
@@ -424,6 +428,7 @@ int mlp_train_step(const mlp_t* h, const void* packed, const uint16_t* X, const 
     a.T = T;
     a.stashA = reinterpret_cast<uint16_t*>(ws + w.stashA);
     a.stashS = h->act == MLP_ACT_SINE ? reinterpret_cast<uint16_t*>(ws + w.stashS) : nullptr;
+    a.reluMask = h->act == MLP_ACT_RELU ? reinterpret_cast<uint32_t*>(ws + w.reluMask) : nullptr;
     a.deltaOut = reinterpret_cast<uint16_t*>(ws + w.deltaOut);
     a.lossPart = reinterpret_cast<float*>(ws + w.lossPart);
     hipError_t e = launch_forward(h->width, h->act, FWD_TRAIN, a, s, &nloss);

@@ -121,9 +121,25 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
       });
     }
 
+    // ReLU: the mask words of the activation a layer needs (stash index
+    // l - 1 for layer l), requested one layer ahead.
+    const size_t mblk = (size_t)(a.M16 / 16);
+    auto mask_rsrc = [&](int idx) {
+      return make_rsrc(a.reluMask + ((size_t)idx * mblk + tb0) * 64, a.reluMask ? (int64_t)vblk * 256 : 0);
+    };
+    uint32_t mw[NT];
+    if constexpr (ACT == ACT_RELU) {
+      if (L > 1) {
+        const rsrc_t mr = mask_rsrc(L - 2);
+#pragma unroll
+        for (int n = 0; n < NT; ++n) mw[n] = bload32(mr, lane * 4, (uint32_t)(n * 256));
+      }
+    }
+
     // Backward layer l: out = bf16((in W_l^T) * sigma'(a_l)), the delta of
     // layer l-1 in chain order; it is also stored for the gradient kernel.
-    // The derivative source of strip s is requested PF strips ahead.
+    // The derivative source of strip s is requested PF strips ahead (ReLU:
+    // the layer's mask words, requested during the previous layer).
     auto layer = [&](int l, const u32x4 (&in)[NT][KBW], u32x4 (&out)[NT][KBW]) {
       const u32x4* wl;
       if (resident) {
@@ -145,8 +161,16 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
       }
       constexpr int PF = SW < 4 ? SW : 4;
       u32x2 gv[SW][NT];
+      uint32_t mwn[NT];
+      if constexpr (ACT == ACT_RELU) {
+        if (l - 1 >= 1) {
+          const rsrc_t mr = mask_rsrc(l - 2);
+#pragma unroll
+          for (int n = 0; n < NT; ++n) mwn[n] = bload32(mr, lane * 4, (uint32_t)(n * 256));
+        }
+      }
       auto request = [&](int s) {
-        if constexpr (ACT != ACT_LINEAR) {
+        if constexpr (ACT != ACT_LINEAR && ACT != ACT_RELU) {
 #pragma unroll
           for (int n = 0; n < NT; ++n) gv[s][n] = bload64(gsrc, lane * 8, (uint32_t)((n * SW + s) * 512));
         }
@@ -173,8 +197,9 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
           uint32_t p0, p1;
           if constexpr (ACT == ACT_RELU) {
             // relu'(a) is [a > 0]; zero the rounded products where a is 0
-            p0 = mask_bf16x2_by_positive(pack_bf16x2(acc[n][0], acc[n][1]), gv[s][n].x);
-            p1 = mask_bf16x2_by_positive(pack_bf16x2(acc[n][2], acc[n][3]), gv[s][n].y);
+            const uint32_t t = mw[n] >> (2 * s);
+            p0 = mask_halves(pack_bf16x2(acc[n][0], acc[n][1]), t & 0x00010001u);
+            p1 = mask_halves(pack_bf16x2(acc[n][2], acc[n][3]), (t >> 1) & 0x00010001u);
           } else if constexpr (ACT == ACT_LINEAR) {
             p0 = pack_bf16x2(acc[n][0], acc[n][1]);
             p1 = pack_bf16x2(acc[n][2], acc[n][3]);
@@ -196,6 +221,10 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
         // Keep each strip's work together: bounds the live registers.
         __builtin_amdgcn_sched_barrier(0);
       });
+      if constexpr (ACT == ACT_RELU) {
+#pragma unroll
+        for (int n = 0; n < NT; ++n) mw[n] = mwn[n];
+      }
       if (!resident) {
         drain_and_sync();  // next layer staged; this buffer free again
         ++step;

@@ -33,6 +33,13 @@
 //    bf16 result registers of a wave, stored as they are.  Element (m, f)
 //    lives at ((m/16 * F/16 + f/16) * 64 + ((f%16)/4) * 16 + m%16) * 4 + f%4.
 //    Every 16-row block of a strip is 64 lanes x 4 values, contiguous.
+//
+//  * ReLU masks ([M16 / 16][64] 32-bit words per hidden activation, ReLU
+//    nets only): the word of lane (g, i) for 16-row block b holds, for
+//    strip s, [A[16 b + i][16 s + 4 g + r] > 0] in bit 2 s + r / 2 + 16 (r % 2)
+//    (r = 0, 2 in the low half, r = 1, 3 in the high half), so one shift
+//    and one AND give the 0/1 multipliers of a packed bf16 pair.  The
+//    backward pass reads these instead of the bf16 activations.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -98,6 +105,7 @@ struct FwdArgs {
   uint16_t* stashS;     // same shape, bf16(cos c) of sine layers, or null
   uint16_t* deltaOut;   // [M16][OP] tile image of the output delta (train)
   float* cOut;          // [M16][OP] fp32 tile image of c_{L-1} (stash mode)
+  uint32_t* reluMask;   // (L-1) x [M16/16][64] ReLU mask words, or null
   float* lossPart;      // one partial sum per workgroup (train)
   int64_t M, M16;
   int in_dim, out_dim, L, out_act;
@@ -114,6 +122,7 @@ struct BwdArgs {
   uint16_t* deltaOut;   // [M16][OP]: delta_{L-1}
   const float* cOut;    // [M16][OP] fp32 (seeded mode, nonlinear output)
   const float* dY;      // [M][out_dim] (seeded mode)
+  const uint32_t* reluMask;  // (L-1) x [M16/16][64] ReLU mask words (ReLU nets)
   int64_t M, M16;
   int out_dim, L, out_act;
   int ntiles, resident;

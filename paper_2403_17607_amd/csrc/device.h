@@ -41,13 +41,18 @@ __device__ __forceinline__ uint32_t relu_bf16x2(uint32_t p) {
   return __builtin_bit_cast(uint32_t, __builtin_elementwise_max(__builtin_bit_cast(s16x2, p), (s16x2){0, 0}));
 }
 
-// Zero each bf16 half of p whose half in a is zero (a holds non-negative bf16
-// values, so "nonzero" is "> 0").  Two packed int16 instructions.
-__device__ __forceinline__ uint32_t mask_bf16x2_by_positive(uint32_t p, uint32_t a) {
-  // the constant 1 in both halves comes from a register: an inline
-  // constant of a packed instruction would give the high half 0
-  uint32_t m, r;
-  asm("v_pk_min_u16 %0, %1, %2" : "=v"(m) : "v"(a), "v"(0x00010001u));
+// Each half of p (a non-negative bf16 value) as 0 or 1 in that half.  The
+// constant 1 in both halves comes from a register: an inline constant of a
+// packed instruction would give the high half 0.
+__device__ __forceinline__ uint32_t nonzero_halves(uint32_t p) {
+  uint32_t m;
+  asm("v_pk_min_u16 %0, %1, %2" : "=v"(m) : "v"(p), "v"(0x00010001u));
+  return m;
+}
+
+// p with each 16-bit half multiplied by the 0 or 1 in the same half of m.
+__device__ __forceinline__ uint32_t mask_halves(uint32_t p, uint32_t m) {
+  uint32_t r;
   asm("v_pk_mul_lo_u16 %0, %1, %2" : "=v"(r) : "v"(p), "v"(m));
   return r;
 }
@@ -117,6 +122,12 @@ __device__ __forceinline__ u32x2 bload64(rsrc_t r, uint32_t voff, uint32_t soff)
 }
 __device__ __forceinline__ u32x4 bload128(rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r, voff, soff, 0));
+}
+__device__ __forceinline__ uint32_t bload32(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
+}
+__device__ __forceinline__ void bstore32(uint32_t v, rsrc_t r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, 0);
 }
 __device__ __forceinline__ void bstore64(u32x2 v, rsrc_t r, uint32_t voff, uint32_t soff) {
   __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, 0);

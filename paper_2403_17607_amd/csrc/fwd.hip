@@ -213,6 +213,11 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       const size_t soff = (size_t)l * a.M16 * W + (size_t)row0 * W;
       const rsrc_t sa = make_rsrc(a.stashA + soff, a.stashA ? (int64_t)vblk * 32 * W : 0);
       const rsrc_t ss = make_rsrc(a.stashS + soff, a.stashS ? (int64_t)vblk * 32 * W : 0);
+      // ReLU mask words of this layer's activation (training, ReLU nets)
+      constexpr bool MASK = MODE != FWD_INFER && ACT == ACT_RELU;
+      uint32_t mk[NT];
+#pragma unroll
+      for (int n = 0; n < NT; ++n) mk[n] = 0u;
       if constexpr (SW == 1) {
         // width 16: the second half of the only k-block is padding
 #pragma unroll
@@ -245,6 +250,10 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
             out[n][s >> 1].x = p0;
             out[n][s >> 1].y = p1;
           }
+          if constexpr (MASK) {
+            mk[n] |= (nonzero_halves(p0) | (nonzero_halves(p1) << 1)) << (2 * s);
+            pin(mk[n]);
+          }
           if constexpr (MODE != FWD_INFER) {
             const uint32_t so = (uint32_t)((n * SW + s) * 512);
             bstore64(u32x2{p0, p1}, sa, lane * 8, so);
@@ -258,6 +267,12 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
         // Keep each strip's work together: bounds the live registers.
         __builtin_amdgcn_sched_barrier(0);
       });
+      if constexpr (MASK) {
+        const rsrc_t mr = make_rsrc(a.reluMask + ((size_t)l * (a.M16 / 16) + tb0) * 64,
+                                    a.reluMask ? (int64_t)vblk * 256 : 0);
+#pragma unroll
+        for (int n = 0; n < NT; ++n) bstore32(mk[n], mr, lane * 4, (uint32_t)(n * 256));
+      }
       if (!resident) {
         drain_and_sync();  // next layer staged; this buffer free again
         ++step;

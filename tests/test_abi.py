@@ -73,8 +73,13 @@ def test_workspace_sizes(ffmlp):
     # at least the activation and delta stashes: 2 x depth x M x width bf16
     assert big >= 2 * 4 * (1 << 20) * 64 * 2
     assert small < big and small % 256 == 0
+    # sine adds the bf16 cos stash; ReLU instead keeps one 32-bit mask word
+    # per lane of every 16-row block and hidden activation
     sine = ffmlp.FusedMLP(64, 4, 64, 16, "sine")
-    assert sine.workspace_bytes(1 << 20) >= big + 4 * (1 << 20) * 64 * 2
+    relu_masks = 4 * ((1 << 20) // 16) * 64 * 4
+    assert sine.workspace_bytes(1 << 20) >= big - relu_masks + 4 * (1 << 20) * 64 * 2
+    lin = ffmlp.FusedMLP(64, 4, 64, 16, "linear")
+    assert big - lin.workspace_bytes(1 << 20) == relu_masks
 
 
 @pytest.mark.parametrize("args,code", [
