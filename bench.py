@@ -7,11 +7,9 @@ One step = the whole path over one synthetic batch of M rows:
 `value` is M / (time per step) in samples/s with inputs resident in HBM.
 
 The `roofline` object is the inference kernel (one launch per forward
-call): algorithmic flops 2 * sum(fan_in * fan_out) per row, over the
-kernel's average launch duration (HIP events on its stream around
-back-to-back launches after the timed steps), against the dense bf16 MFMA
-peak.  `infer.ms` is the per-step event time of the same launch, which
-also holds its dispatch latency.
+call, so HIP events on its stream around it in every timed step time
+exactly that launch): algorithmic flops 2 * sum(fan_in * fan_out) per row
+against the dense bf16 MFMA peak.
 `roofline_train` is the whole training step against HBM bandwidth, with
 its algorithmic bytes per row.  `cpu_baseline` times the fp64 oracle on a
 bounded sample of the same step on the host cores.
@@ -184,19 +182,6 @@ def main():
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
 
-    # Average duration of one inference launch, for the roofline: R
-    # back-to-back launches between two events on the launch stream (no
-    # marker between launches, so each dispatch overlaps the kernel before
-    # it and the average is the kernel's own duration).
-    R = max(K, 10)
-    k0, k1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    k0.record(stream)
-    for i in range(R):
-        net.forward(packed, Xs[i % 2], Y=Y)
-    k1.record(stream)
-    torch.cuda.synchronize()
-    t_inf_kernel = k0.elapsed_time(k1) / R  # ms
-
     t_step = sum(e[0].elapsed_time(e[3]) for e in ev) / K  # ms
     t_inf = sum(e[1].elapsed_time(e[2]) for e in ev) / K
     t_train = sum(e[2].elapsed_time(e[3]) for e in ev) / K
@@ -205,7 +190,6 @@ def main():
 
     fl_inf, fl_train = flops_per_row(width, depth, in_dim, out_dim)
     inf_tflops = fl_inf * M / (t_inf * 1e-3) / 1e12
-    kern_tflops = fl_inf * M / (t_inf_kernel * 1e-3) / 1e12
     train_tflops = fl_train * M / (t_train * 1e-3) / 1e12
     bytes_inf = M * (2 * in_dim + 2 * out_dim)
     bytes_train = M * train_bytes_per_row(width, depth, in_dim, out_dim, args.act)
@@ -238,10 +222,9 @@ def main():
         "pack_ms": t_pack,
         "event_ms_per_step": t_step,
         "roofline": {"kernel": "fwd_kernel (inference)", "bound": "mfma",
-                     "achieved": kern_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                     "frac": kern_tflops / PEAK_BF16_TFLOPS,
-                     "launch_us": t_inf_kernel * 1e3,
-                     "launch_us_method": f"HIP events around {R} back-to-back launches",
+                     "achieved": inf_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                     "frac": inf_tflops / PEAK_BF16_TFLOPS,
+                     "launch_us": t_inf * 1e3,
                      "traffic": measured_traffic(
                          f"fwd_infer_w{width}_d{depth}_in{in_dim}_out{out_dim}_{args.act}_b{M}")
                      if args.out_act == "linear" else None,
