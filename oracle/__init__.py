@@ -70,9 +70,10 @@ def _load():
         lib.orc_param_count.restype = ctypes.c_int64
         lib.orc_forward.argtypes = [np_, dp, dp, ctypes.c_int64, dp, dp, dp]
         lib.orc_backward.argtypes = [np_, dp, dp, ctypes.c_int64, dp, dp, dp]
+        lib.orc_backward_dx.argtypes = [np_, dp, dp, ctypes.c_int64, dp, dp, dp, dp]
         lib.orc_train_step.argtypes = [np_, dp, dp, dp, ctypes.c_int64, dp, dp,
                                        dp, dp, dp]
-        for f in (lib.orc_forward, lib.orc_backward, lib.orc_train_step):
+        for f in (lib.orc_forward, lib.orc_backward, lib.orc_backward_dx, lib.orc_train_step):
             f.restype = ctypes.c_int
         _lib = lib
     return _lib
@@ -165,6 +166,20 @@ class Net:
         if rc != 0:
             raise ValueError("orc_backward rejected its arguments")
         return (G, self._deltas(D, M)) if want_deltas else G
+
+    def backward_dx(self, W, X, dY):
+        """backward() plus the input gradient: returns (G, dX), dX [M, in_dim]
+        fp64, the first hidden layer's delta times W_1^T (no rounding)."""
+        W, X, dY = _f64(W), _f64(X), _f64(dY)
+        M = X.shape[0]
+        assert dY.shape == (M, self.out_dim)
+        G = np.zeros(self.param_count())
+        dX = np.zeros((M, self.in_dim))
+        rc = _load().orc_backward_dx(ctypes.byref(self._c()), _ptr(W), _ptr(X), M,
+                                     _ptr(dY), _ptr(G), None, _ptr(dX))
+        if rc != 0:
+            raise ValueError("orc_backward_dx rejected its arguments")
+        return G, dX
 
     def train_step(self, W, X, T, want_deltas: bool = False):
         """Algorithm 2 with the MSE loss.  Returns dict with Y, Y32, G (flat),

@@ -176,7 +176,7 @@ static void forward_row(const orc_net* n, const double* W, const double* x,
  * adds the row's contribution A_l^T D_{l+1} to G (fp64).
  */
 static void backward_row(const orc_net* n, const double* W, const double* g,
-                         row_buf* b, double* G) {
+                         row_buf* b, double* G, double* dx) {
   const int L = n_layers(n), D = max_dim(n);
   /* Output delta: D_{L+1} = sigma_b(Y, g). */
   {
@@ -199,6 +199,18 @@ static void backward_row(const orc_net* n, const double* W, const double* g,
       const double ak = a[k];
       double* grow = Gl + (size_t)k * fo;
       for (int j = 0; j < fo; ++j) grow[j] += ak * dn[j];
+    }
+    /* The input gradient (an extension beyond Algorithm 2, which stops at
+     * the first hidden layer): X enters the first product linearly, so
+     * dLoss/dX = D_1 W_1^T (1-based), with no activation derivative and no
+     * rounding. */
+    if (l == 0 && dx) {
+      for (int k = 0; k < fi; ++k) {
+        const double* wrow = Wl + (size_t)k * fo;
+        double p = 0.0;
+        for (int j = 0; j < fo; ++j) p += dn[j] * wrow[j];
+        dx[k] = p;
+      }
     }
     /* D_l = sigma_b(A_l, D_{l+1} W_l^T), only down to l = 2 (1-based):
      * the input layer gets no delta. */
@@ -276,7 +288,7 @@ int orc_forward(const orc_net* n, const double* W, const double* X,
 static int run_backward(const orc_net* n, const double* W, const double* X,
                         const double* T, const double* dY, int64_t M,
                         double* Y, double* Y32, double* G, double* loss,
-                        double* Dout) {
+                        double* Dout, double* dX) {
   const int64_t P = orc_param_count(n);
   const int nt = thread_count(n);
   double* partial = (double*)calloc((size_t)nt * P, sizeof(double));
@@ -313,7 +325,7 @@ static int run_backward(const orc_net* n, const double* W, const double* X,
         } else {
           for (int j = 0; j < n->out_dim; ++j) g[j] = dY[r * n->out_dim + j];
         }
-        backward_row(n, W, g, &b, Gt);
+        backward_row(n, W, g, &b, Gt, dX ? dX + r * n->in_dim : NULL);
         store_row_outputs(n, &b, M, r, Y, Y32, NULL);
         if (Dout) store_row_deltas(n, &b, M, r, Dout);
       }
@@ -338,13 +350,19 @@ static int run_backward(const orc_net* n, const double* W, const double* X,
 
 int orc_backward(const orc_net* n, const double* W, const double* X,
                  int64_t M, const double* dY, double* G, double* D) {
+  return orc_backward_dx(n, W, X, M, dY, G, D, NULL);
+}
+
+int orc_backward_dx(const orc_net* n, const double* W, const double* X,
+                    int64_t M, const double* dY, double* G, double* D,
+                    double* dX) {
   if (check_net(n, M) || !W || !G || (M > 0 && (!X || !dY))) return -1;
-  return run_backward(n, W, X, NULL, dY, M, NULL, NULL, G, NULL, D);
+  return run_backward(n, W, X, NULL, dY, M, NULL, NULL, G, NULL, D, dX);
 }
 
 int orc_train_step(const orc_net* n, const double* W, const double* X,
                    const double* T, int64_t M, double* Y, double* Y32,
                    double* G, double* loss, double* D) {
   if (check_net(n, M) || !W || !G || (M > 0 && (!X || !T))) return -1;
-  return run_backward(n, W, X, T, NULL, M, Y, Y32, G, loss, D);
+  return run_backward(n, W, X, T, NULL, M, Y, Y32, G, loss, D, NULL);
 }

@@ -84,6 +84,15 @@ int orc_backward(const orc_net* n, const double* W, const double* X,
                  int64_t M, const double* dY, double* G, double* D);
 
 /*
+ * orc_backward plus the input gradient dX = dLoss/dX [M, in_dim], the
+ * product of the first hidden layer's delta with the first weight
+ * matrix's transpose, unrounded (dX may be NULL).
+ */
+int orc_backward_dx(const orc_net* n, const double* W, const double* X,
+                    int64_t M, const double* dY, double* G, double* D,
+                    double* dX);
+
+/*
  * One training step of Algorithm 2 with the mean-squared-error loss:
  * Y and Y32 as in orc_forward (Y32 may be NULL), G and D as in
  * orc_backward, *loss = sum (Y32 - T)^2 / (M out_dim) (loss may be NULL).

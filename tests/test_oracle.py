@@ -256,6 +256,88 @@ def test_gradient_matches_finite_differences(case):
     np.testing.assert_allclose(Gb, fdb, rtol=1e-6, atol=1e-8 * np.max(np.abs(Gb)))
 
 
+# ----------------------------------------------------------- input gradient
+
+@pytest.mark.parametrize("case", FD_CASES)
+def test_input_gradient_matches_finite_differences(case):
+    """dX (an extension beyond Algorithm 2) is the gradient of sum(dY * Y)
+    with respect to X, checked by central differences with rounding off;
+    G from backward_dx equals G from backward."""
+    width, depth, in_dim, out_dim, act, out_act = case
+    net = Net(width, depth, in_dim, out_dim, act, out_act, round_bf16=False)
+    rng = np.random.default_rng((hash(case) + 7) % 2**32)
+    M = 5
+    W = rng.uniform(-1, 1, net.param_count())
+    X = rng.uniform(-1, 1, (M, in_dim))
+    if act == RELU:
+        for _ in range(100):
+            Xb, ok = X.copy(), True
+            for Wl in net.split(W)[:-1]:
+                C = Xb @ Wl
+                ok = ok and np.min(np.abs(C)) >= 1e-3
+                Xb = np.maximum(C, 0)
+            if ok:
+                break
+            X = rng.uniform(-1, 1, (M, in_dim))
+        assert ok
+    dY = rng.uniform(-1, 1, (M, out_dim))
+    G, dX = net.backward_dx(W, X, dY)
+    np.testing.assert_array_equal(G, net.backward(W, X, dY))
+    h = 1e-6
+    fd = np.zeros_like(X)
+    for r in range(M):
+        for k in range(in_dim):
+            Xp, Xm = X.copy(), X.copy()
+            Xp[r, k] += h
+            Xm[r, k] -= h
+            fd[r, k] = (np.sum(dY * net.forward(W, Xp)[1]) - np.sum(dY * net.forward(W, Xm)[1])) / (2 * h)
+    np.testing.assert_allclose(dX, fd, rtol=1e-6, atol=1e-8 * np.max(np.abs(dX)))
+
+
+@pytest.mark.parametrize("out_act", [LINEAR, SIGMOID])
+def test_depth0_input_gradient_is_one_gemm(out_act):
+    """Depth 0, no rounding: dX = (dY * sigma_out'(C)) W^T, one library
+    matmul."""
+    net = Net(width=32, depth=0, in_dim=20, out_dim=12, out_act=out_act, round_bf16=False)
+    W, X, _ = rand_net_inputs(net, 129)
+    dY = RNG.uniform(-1, 1, (129, 12))
+    _, dX = net.backward_dx(W, X, dY)
+    Wm = W.reshape(20, 12)
+    D = dY
+    if out_act == SIGMOID:
+        Y = 1 / (1 + np.exp(-(X @ Wm)))
+        D = dY * Y * (1 - Y)
+    np.testing.assert_allclose(dX, D @ Wm.T, rtol=1e-12, atol=1e-15)
+
+
+def test_identity_net_input_gradient_closed_form():
+    """Identity weights, ReLU hidden, linear output, rounding on: every
+    hidden delta is bf16(dY) masked by [X > 0], so dX = bf16(dY) [X > 0]
+    exactly."""
+    w, depth, M = 8, 3, 16
+    net = Net(width=w, depth=depth, in_dim=w, out_dim=w)
+    W = np.concatenate([np.eye(w).ravel()] * net.L)
+    _, X, _ = rand_net_inputs(net, M)
+    dY = RNG.uniform(-1, 1, (M, w))
+    _, dX = net.backward_dx(W, X, dY)
+    rne = np.vectorize(oracle.rne_bf16)
+    np.testing.assert_array_equal(dX, rne(dY) * (X > 0))
+
+
+def test_input_gradient_is_unrounded_product_of_first_delta():
+    """Rounding on: dX is the first hidden layer's (rounded, separately
+    pinned) delta times W_1^T, kept in fp64 (not rounded to bf16)."""
+    net = Net(width=16, depth=2, in_dim=12, out_dim=5, act=SIGMOID)
+    W, X, _ = rand_net_inputs(net, 40)
+    dY = RNG.uniform(-1, 1, (40, 5))
+    G, D = net.backward(W, X, dY, want_deltas=True)
+    _, dX = net.backward_dx(W, X, dY)
+    ref = D[0] @ net.split(W)[0].T
+    np.testing.assert_allclose(dX, ref, rtol=1e-13, atol=1e-18)
+    rne = np.vectorize(oracle.rne_bf16)
+    assert np.any(rne(dX) != dX)
+
+
 # ------------------------------------------------------- closed-form deltas
 
 def test_identity_net_deltas_closed_form():
