@@ -138,6 +138,18 @@ int mlp_backward(const mlp_t* h, const void* packed, const uint16_t* X,
                  const float* dY, float* G, int64_t M, void* ws,
                  void* stream);
 
+/* mlp_backward plus the input gradient dX = dLoss/dX (an extension beyond
+ * Algorithm 2 of section III-A, which stops at the first hidden layer: X
+ * enters the first product linearly, so dX = D_1 W_1^T in 1-based layer
+ * numbering, with no activation derivative).
+ *   dX  fp32 [M][in_dim] row-major, 16-byte aligned, written in full (not
+ *       rounded to bf16); the other arguments as for mlp_backward.
+ * A caller chaining nets passes dX of one net as dY of the net before it.
+ * Same error behaviour as mlp_backward; dX == NULL is mlp_backward. */
+int mlp_backward_dx(const mlp_t* h, const void* packed, const uint16_t* X,
+                    const float* dY, float* G, float* dX, int64_t M, void* ws,
+                    void* stream);
+
 /*
  * One training step, Algorithm 2: forward with stash, mean-squared-error
  * loss over the M * out_dim outputs, output delta 2 (Y - T) / (M out_dim)

@@ -58,6 +58,7 @@ _SIGNATURES = {
     "mlp_workspace_bytes": (ctypes.c_size_t, [_VP, ctypes.c_int64, ctypes.c_int]),
     "mlp_forward": (ctypes.c_int, [_VP, _VP, _VP, _VP, ctypes.c_int64, _VP, _VP]),
     "mlp_backward": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, ctypes.c_int64, _VP, _VP]),
+    "mlp_backward_dx": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_int64, _VP, _VP]),
     "mlp_train_step": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_int64,
                                       _VP, _VP]),
     "mlp_last_error": (ctypes.c_char_p, []),
@@ -199,6 +200,22 @@ class FusedMLP:
         _check(lib().mlp_backward(self._h, _ptr(packed), _ptr(X), _ptr(dY), _ptr(G), X.shape[0],
                                   _ptr(ws), _stream(X.device)))
         return G
+
+    def backward_dx(self, packed: torch.Tensor, X: torch.Tensor, dY: torch.Tensor,
+                    ws: torch.Tensor, G: torch.Tensor | None = None,
+                    dX: torch.Tensor | None = None):
+        """backward() plus the input gradient dX (fp32 [M, in_dim]); returns
+        (G, dX)."""
+        assert dY.dtype == torch.float32 and dY.shape == (X.shape[0], self.out_dim)
+        M = X.shape[0]
+        if G is None:
+            G = torch.empty(self.param_count(), dtype=torch.float32, device=X.device)
+        if dX is None:
+            dX = torch.empty(M, self.in_dim, dtype=torch.float32, device=X.device)
+        assert dX.dtype == torch.float32 and dX.shape == (M, self.in_dim) and dX.is_contiguous()
+        _check(lib().mlp_backward_dx(self._h, _ptr(packed), _ptr(X), _ptr(dY), _ptr(G), _ptr(dX),
+                                     M, _ptr(ws), _stream(X.device)))
+        return G, dX
 
     def train_step(self, packed: torch.Tensor, X: torch.Tensor, T: torch.Tensor,
                    ws: torch.Tensor, G: torch.Tensor | None = None, Y: torch.Tensor | None = None,

@@ -48,10 +48,11 @@ int kblocks(int n) { return (n + 31) / 32; }
 int strips(int n) { return (n + 15) / 16; }
 
 // Fragment counts of the packed buffer: forward layers 0 .. L-1, then
-// backward layers 1 .. L-1.
+// backward layers 1 .. L-1, then backward layer 0 (input gradient only).
 struct PackGeom {
   uint32_t fwd_frag[2], fwd_total;  // [0] = layer 0, [1] = hidden layers
-  uint32_t bwd_hidden, bwd_total;
+  uint32_t bwd_hidden, bwd_total;   // backward layers 1 .. L-1
+  uint32_t bwd0;                    // backward layer 0, after them
 };
 
 PackGeom pack_geom(const mlp* h) {
@@ -72,6 +73,7 @@ PackGeom pack_geom(const mlp* h) {
   for (int l = 1; l < L; ++l) bt += (uint32_t)strips(fan_in_of(h, l)) * kblocks(W);
   g.bwd_hidden = (uint32_t)strips(W) * kblocks(W);
   g.bwd_total = bt;
+  g.bwd0 = (uint32_t)strips(h->in_dim) * kblocks(W);
   return g;
 }
 
@@ -159,6 +161,7 @@ BwdArgs bwd_args(const mlp* h, const void* packed, const WsLayout& w, uint8_t* w
   b.reluMask = h->act == MLP_ACT_RELU ? reinterpret_cast<const uint32_t*>(ws + w.reluMask) : nullptr;
   b.M = M;
   b.M16 = w.M16;
+  b.in_dim = h->in_dim;
   b.out_dim = h->out_dim;
   b.L = n_mats(h);
   b.out_act = h->out_act;
@@ -166,6 +169,9 @@ BwdArgs bwd_args(const mlp* h, const void* packed, const WsLayout& w, uint8_t* w
   b.ntiles = (int)((M + rows - 1) / rows);
   b.layH_frags = g.bwd_hidden;
   b.total_frags = g.bwd_total;
+  b.packed0 = reinterpret_cast<const u32x4*>(static_cast<const uint8_t*>(packed) +
+                                             (size_t)(g.fwd_total + g.bwd_total) * 1024);
+  b.dX = nullptr;
   return b;
 }
 
@@ -328,7 +334,7 @@ int mlp_layer_shape(const mlp_t* h, int l, int* fan_in, int* fan_out, int64_t* o
 size_t mlp_packed_bytes(const mlp_t* h) {
   if (!h) return 0;
   const PackGeom g = pack_geom(h);
-  return (size_t)(g.fwd_total + g.bwd_total) * 1024;
+  return (size_t)(g.fwd_total + g.bwd_total + g.bwd0) * 1024;
 }
 
 int mlp_pack_weights(const mlp_t* h, const uint16_t* W, void* packed, void* stream) {
@@ -386,13 +392,19 @@ int mlp_forward(const mlp_t* h, const void* packed, const uint16_t* X, uint16_t*
 
 int mlp_backward(const mlp_t* h, const void* packed, const uint16_t* X, const float* dY, float* G,
                  int64_t M, void* ws_, void* stream) {
+  return mlp_backward_dx(h, packed, X, dY, G, nullptr, M, ws_, stream);
+}
+
+int mlp_backward_dx(const mlp_t* h, const void* packed, const uint16_t* X, const float* dY,
+                    float* G, float* dX, int64_t M, void* ws_, void* stream) {
   g_err.clear();
   if (int rc = check_handle(h)) return rc;
   if (M < 0) return fail(MLP_ERR_INVALID_ARG, "M = %lld < 0", (long long)M);
   if (!G || !ws_) return fail(MLP_ERR_INVALID_ARG, "null G or workspace");
   if (M > 0 && (!packed || !X || !dY)) return fail(MLP_ERR_INVALID_ARG, "null packed, X or dY");
-  if (!aligned(G, 4) || !aligned(ws_, 256) || (M > 0 && (!aligned(packed, 16) || !aligned(X, 16) || !aligned(dY, 16))))
-    return fail(MLP_ERR_INVALID_ARG, "misaligned pointer (packed, X, dY: 16 bytes; ws: 256; G: 4)");
+  if (!aligned(G, 4) || !aligned(ws_, 256) ||
+      (M > 0 && (!aligned(packed, 16) || !aligned(X, 16) || !aligned(dY, 16) || (dX && !aligned(dX, 16)))))
+    return fail(MLP_ERR_INVALID_ARG, "misaligned pointer (packed, X, dY, dX: 16 bytes; ws: 256; G: 4)");
   if (M > ((int64_t)1 << 36)) return fail(MLP_ERR_INVALID_ARG, "M > 2^36");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const WsLayout w = ws_layout(h, M);
@@ -400,6 +412,7 @@ int mlp_backward(const mlp_t* h, const void* packed, const uint16_t* X, const fl
   if (M > 0) {
     BwdArgs b = bwd_args(h, packed, w, ws, M);
     b.dY = dY;
+    b.dX = dX;
     hipError_t e = launch_backward(h->width, h->act, 1, b, s);
     if (e != hipSuccess) return hip_fail(e, "backward kernel launch");
   }

@@ -19,7 +19,7 @@ namespace ffmlp {
 // RES: every layer's weights resident in LDS (else staged layer by layer);
 // each mode is its own kernel, so the tile loop carries no residency
 // branches (whose joins force conservative waits on LDS loads).
-template <int W, int ACT, int SEEDED, bool RES>
+template <int W, int ACT, int SEEDED, bool RES, bool DX>
 __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs a) {
   constexpr int NT = TileCfg<W>::NT, NW = TileCfg<W>::NW;
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
@@ -231,13 +231,56 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
       }
     };
 
+    // Input gradient (DX; an extension beyond Algorithm 2): dX^T = W_1 D_1^T
+    // (1-based), no activation derivative, fp32 out.  The backward-packed
+    // first layer is read straight from global memory (L2), not from LDS:
+    // it is needed once per tile and would push the resident set past LDS.
+    auto input_grad = [&](const u32x4 (&in)[NT][KBW]) {
+      const int in_dim = a.in_dim;
+      const int SI = (in_dim + 15) >> 4;
+      const bool xv = (in_dim & 3) == 0;
+      const rsrc_t xr = make_rsrc(a.dX + row0 * in_dim, vrows * in_dim * 4);
+      for (int s = 0; s < SI; ++s) {
+        u32x4 af[KBW];
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) af[kb] = a.packed0[(s * KBW + kb) * 64 + lane];
+        f32x4 acc[NT];
+#pragma unroll
+        for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb)
+#pragma unroll
+          for (int n = 0; n < NT; ++n) acc[n] = mfma16(af[kb], in[n][kb], acc[n]);
+        const int f0 = 16 * s + 4 * lg;
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+          if (xv) {
+            const uint32_t eo = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 4) : kOOB;
+            bstore128(__builtin_bit_cast(u32x4, acc[n]), xr, eo, (uint32_t)(n * 16 * in_dim * 4));
+          } else {
+            const int64_t m = row0 + n * 16 + li;
+            if (m < M) {
+#pragma unroll
+              for (int r = 0; r < 4; ++r)
+                if (f0 + r < in_dim) a.dX[m * in_dim + f0 + r] = acc[n][r];
+            }
+          }
+        }
+      }
+    };
+
     // Layers in pairs with two delta buffers, so no register array is copied.
     int l = L - 1;
     for (; l - 2 >= 0; l -= 2) {
       layer(l, dA, dB);
       layer(l - 1, dB, dA);
     }
-    if (l >= 1) layer(l, dA, dB);
+    if (l >= 1) {
+      layer(l, dA, dB);
+      if constexpr (DX) input_grad(dB);
+    } else {
+      if constexpr (DX) input_grad(dA);
+    }
   }
 }
 
@@ -252,7 +295,11 @@ static hipError_t launch_t(const BwdArgs& a0, hipStream_t stream) {
   a.resident = res_bytes + 1024 <= (size_t)di.max_lds ? 1 : 0;
   size_t lds = a.resident ? res_bytes : (size_t)2 * a.layH_frags * 1024;
   if (lds == 0) lds = 16;
-  auto kern = a.resident ? bwd_kernel<W, ACT, SEEDED, true> : bwd_kernel<W, ACT, SEEDED, false>;
+  auto kern = a.resident ? bwd_kernel<W, ACT, SEEDED, true, false> : bwd_kernel<W, ACT, SEEDED, false, false>;
+  if constexpr (SEEDED) {
+    if (a.dX != nullptr)
+      kern = a.resident ? bwd_kernel<W, ACT, SEEDED, true, true> : bwd_kernel<W, ACT, SEEDED, false, true>;
+  }
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), NTH, lds, &occ);
   if (e != hipSuccess) return e;

@@ -123,8 +123,10 @@ struct BwdArgs {
   const float* cOut;    // [M16][OP] fp32 (seeded mode, nonlinear output)
   const float* dY;      // [M][out_dim] (seeded mode)
   const uint32_t* reluMask;  // (L-1) x [M16/16][64] ReLU mask words (ReLU nets)
+  const u32x4* packed0;  // backward-packed layer 0 (input gradient), read from global
+  float* dX;             // [M][in_dim] input gradient, or null
   int64_t M, M16;
-  int out_dim, L, out_act;
+  int in_dim, out_dim, L, out_act;
   int ntiles, resident;
   uint32_t layH_frags, total_frags;
 };

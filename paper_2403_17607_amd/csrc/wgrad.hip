@@ -297,7 +297,8 @@ __global__ __launch_bounds__(256) void reduce2_kernel(const ReduceArgs a) {
 }
 
 // One thread per packed bf16 element.  The buffer holds the forward
-// layers 0 .. L-1, then the backward layers 1 .. L-1, each as fragments
+// layers 0 .. L-1, then the backward layers 1 .. L-1, then the backward
+// layer 0 (for the input gradient), each as fragments
 // [strip][k-block][lane][slot]; see common.h for the two orientations and
 // the contraction orders.
 __global__ __launch_bounds__(256) void pack_kernel(const PackArgs a) {
@@ -306,20 +307,32 @@ __global__ __launch_bounds__(256) void pack_kernel(const PackArgs a) {
   const int Wd = a.width, L = a.L;
   auto fan_in = [&](int l) { return l == 0 ? a.in_dim : Wd; };
   auto fan_out = [&](int l) { return l == L - 1 ? a.out_dim : Wd; };
-  // locate the layer and orientation of element e0
-  int64_t e = e0, woff = 0;
+  // locate the layer and orientation of element e0: forward layers
+  // 0 .. L-1, backward layers 1 .. L-1, then backward layer 0 (read only
+  // by the input-gradient step)
+  int64_t e = e0;
   int dir = 0, l = 0;
-  for (;; ++l) {
-    if (l == L) { dir = 1; l = 1; woff = (int64_t)fan_in(0) * fan_out(0); }
-    if (l >= L) return;  // not reached: e0 < total
+  for (int seg = 0;; ++seg) {
+    if (seg < L) {
+      dir = 0;
+      l = seg;
+    } else if (seg < 2 * L - 1) {
+      dir = 1;
+      l = seg - L + 1;
+    } else if (seg == 2 * L - 1) {
+      dir = 1;
+      l = 0;
+    } else {
+      return;  // not reached: e0 < total
+    }
     const int fi = fan_in(l), fo = fan_out(l);
     const int rows = dir == 0 ? fo : fi;
     const int64_t n = (int64_t)((rows + 15) / 16) * ((Wd + 31) / 32) * 512;
     if (e < n) break;
     e -= n;
-    woff += (int64_t)fi * fo;
-    if (dir == 1 && l == L - 1) return;
   }
+  int64_t woff = 0;
+  for (int k = 0; k < l; ++k) woff += (int64_t)fan_in(k) * fan_out(k);
   const int fi = fan_in(l), fo = fan_out(l);
   const int kblocks = (Wd + 31) / 32;  // every layer is padded to the width's k-blocks
   const int slot = (int)(e & 7), lane = (int)((e >> 3) & 63);

@@ -20,7 +20,7 @@ def declared_functions():
 
 def test_header_declares_the_boundary():
     names = declared_functions()
-    for required in ["mlp_create", "mlp_forward", "mlp_backward", "mlp_train_step",
+    for required in ["mlp_create", "mlp_forward", "mlp_backward", "mlp_backward_dx", "mlp_train_step",
                      "mlp_pack_weights", "mlp_workspace_bytes", "mlp_destroy"]:
         assert required in names
 
@@ -49,12 +49,13 @@ def test_shapes_and_offsets(ffmlp, width):
     assert offs == [0, in_dim * width, in_dim * width + width * width,
                     in_dim * width + 2 * width * width]
     assert net.param_count() == offs[-1] + width * out_dim
-    # packed: forward strips(fan_out) + backward layers 1..L-1 strips(fan_in),
+    # packed: forward strips(fan_out) + backward layers 1..L-1 and 0 strips(fan_in),
     # each with the width's k-blocks, 1 KiB per fragment.
     st = lambda n: (n + 15) // 16
     kb = (width + 31) // 32
     fwd = sum(st(fo) * kb for fi, fo, _ in shapes)
     bwd = sum(st(fi) * kb for fi, fo, _ in shapes[1:])
+    bwd += st(shapes[0][0]) * kb  # backward layer 0, for the input gradient
     assert net.packed_bytes() == (fwd + bwd) * 1024
 
 

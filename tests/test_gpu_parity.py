@@ -13,7 +13,7 @@ import pytest
 import torch
 
 import datagen
-from helpers import (LOSS_TOL, check_grads, check_outputs, f64, inputs, oracle_net)
+from helpers import (LOSS_TOL, check_dx, check_grads, check_outputs, f64, inputs, oracle_net)
 
 pytestmark = pytest.mark.gpu
 
@@ -195,6 +195,77 @@ def test_empty_batch(ffmlp, gpu):
     assert net.forward(packed, X).shape == (0, 16)
 
 
+# ----------------------------------------------------- input gradient dX --
+
+def dx_case(ffmlp, dev, width, depth, in_dim, out_dim, M, act="relu", out_act="linear", seed=21):
+    log(f"dx case w={width} d={depth} in={in_dim} out={out_dim} M={M} act={act} out={out_act}")
+    W, X, _ = inputs(seed, width, depth, in_dim, out_dim, M)
+    dY = datagen.uniform(seed, datagen.STREAM_AUX, (M, out_dim))
+    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, act, out_act)
+    onet = oracle_net(width, depth, in_dim, out_dim, act, out_act)
+    packed = net.pack(W.to(dev))
+    ws = net.workspace(M, dev)
+    Xd, dYd = X.to(dev), dY.to(dev)
+    net.forward(packed, Xd, stash=ws)
+    G, dX = net.backward_dx(packed, Xd, dYd, ws)
+    G0 = net.backward(packed, Xd, dYd, ws)
+    torch.cuda.synchronize()
+    assert torch.equal(G, G0), "G differs between mlp_backward_dx and mlp_backward"
+    Gref, dXref = onet.backward_dx(W, X, dY)
+    log("  dx errs", check_dx(f64(dX), dXref, onet.L))
+    check_grads(f64(G), Gref, onet)
+
+
+@pytest.mark.parametrize("width,depth,in_dim,out_dim,act,out_act", [
+    (16, 2, 16, 16, "relu", "linear"), (32, 3, 32, 7, "sine", "sigmoid"),
+    (64, 4, 64, 16, "relu", "linear"), (128, 4, 128, 16, "relu", "linear"),
+    (128, 1, 100, 3, "sigmoid", "linear"), (64, 0, 40, 12, "linear", "sigmoid"),
+    (64, 2, 3, 1, "sine", "linear"), (128, 5, 127, 33, "relu", "relu")])
+def test_input_gradient(ffmlp, gpu, width, depth, in_dim, out_dim, act, out_act):
+    """dX = D_1 W_1^T against the oracle, G unchanged by asking for dX;
+    both delta-buffer parities, depth 0, in_dim not a multiple of 4."""
+    dx_case(ffmlp, gpu, width, depth, in_dim, out_dim, 4097, act, out_act)
+
+
+def test_input_gradient_streaming(ffmlp, gpu):
+    """Weights too large for LDS (staged layer by layer) with dX."""
+    dx_case(ffmlp, gpu, 128, 16, 128, 128, 3000)
+
+
+def test_chained_nets_nerf_like(ffmlp, gpu):
+    """A density net (in 32 Gaussian features, width 64, 1 hidden layer,
+    16 linear outputs) feeds a color net (its 16 outputs + 16 direction
+    features, width 64, 2 hidden layers, 3 sigmoid outputs).  The color
+    net's dX, first 16 columns, seeds the density net's backward pass;
+    the density net's G matches the oracle's chain."""
+    M = 4096
+    Xd = datagen.gaussian_features(5, datagen.STREAM_X, M, 32)
+    dirs = datagen.gaussian_features(5, datagen.STREAM_AUX, M, 16)
+    Wd = datagen.xavier_weights(5, 64, 1, 32, 16)
+    Wc = datagen.xavier_weights(6, 64, 2, 32, 3)
+    dYc = datagen.uniform(5, datagen.STREAM_T, (M, 3))
+    dens = ffmlp.FusedMLP(64, 1, 32, 16, "relu", "linear")
+    col = ffmlp.FusedMLP(64, 2, 32, 3, "relu", "sigmoid")
+    odens = oracle_net(64, 1, 32, 16, "relu", "linear")
+    ocol = oracle_net(64, 2, 32, 3, "relu", "sigmoid")
+    pd, pc = dens.pack(Wd.to(gpu)), col.pack(Wc.to(gpu))
+    wsd, wsc = dens.workspace(M, gpu), col.workspace(M, gpu)
+    Yd = dens.forward(pd, Xd.to(gpu), stash=wsd)
+    Xc = torch.cat([Yd, dirs.to(gpu)], dim=1).contiguous()
+    col.forward(pc, Xc, stash=wsc)
+    Gc, dXc = col.backward_dx(pc, Xc, dYc.to(gpu), wsc)
+    Gd = dens.backward(pd, Xd.to(gpu), dXc[:, :16].contiguous(), wsd)
+    torch.cuda.synchronize()
+    Yd_ref, _ = odens.forward(Wd, Xd)
+    Xc_ref = np.concatenate([Yd_ref, f64(dirs)], axis=1)
+    Gc_ref, dXc_ref = ocol.backward_dx(Wc, Xc_ref, dYc)
+    Gd_ref = odens.backward(Wd, Xd, dXc_ref[:, :16])
+    check_outputs(f64(Yd), Yd_ref, odens.L)
+    log("  color dx errs", check_dx(f64(dXc), dXc_ref, ocol.L))
+    check_grads(f64(Gc), Gc_ref, ocol)
+    log("  density grad errs", ["%.2e" % e for e in check_grads(f64(Gd), Gd_ref, odens)])
+
+
 # ------------------------------------------- full sizes, sampled rows only --
 
 def sampled_rows(M, n, seed):
@@ -213,9 +284,10 @@ def sampled_rows(M, n, seed):
 ])
 def test_full_size_sampled(ffmlp, gpu, width, depth, in_dim, out_dim, M):
     """At benchmark sizes: Y on sampled rows against the oracle, inference Y
-    bitwise equal to the stashing forward's on every row, and G from
-    mlp_backward with dY nonzero only on the sampled rows (G is a sum over
-    rows, so the oracle needs only those rows)."""
+    bitwise equal to the stashing forward's on every row, and G and dX from
+    mlp_backward_dx with dY nonzero only on the sampled rows (G is a sum
+    over rows and dX a function of each row, so the oracle needs only those
+    rows; every other row's dX is exactly 0)."""
     log(f"full-size w={width} d={depth} M={M}")
     net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, "relu")
     onet = oracle_net(width, depth, in_dim, out_dim, "relu")
@@ -235,11 +307,16 @@ def test_full_size_sampled(ffmlp, gpu, width, depth, in_dim, out_dim, M):
     dYs = datagen.uniform(14, datagen.STREAM_AUX, (len(rows), out_dim))
     dY = torch.zeros(M, out_dim, dtype=torch.float32, device=gpu)
     dY[rows.to(gpu)] = dYs.to(gpu)
-    G = net.backward(packed, Xd, dY, ws)
+    G, dX = net.backward_dx(packed, Xd, dY, ws)
     Yref, _ = onet.forward(W, Xs)
     log("  output errs", check_outputs(f64(Y[rows.to(gpu)]), Yref, onet.L))
-    Gref = onet.backward(W, Xs, dYs)
+    Gref, dXref = onet.backward_dx(W, Xs, dYs)
     errs = check_grads(f64(G), Gref, onet)
+    log("  dx errs", check_dx(f64(dX[rows.to(gpu)]), dXref, onet.L))
+    # rows with dY = 0 have dX = 0 exactly
+    others = torch.ones(M, dtype=torch.bool, device=gpu)
+    others[rows.to(gpu)] = False
+    assert torch.count_nonzero(dX[others]).item() == 0
     log("  grad errs", ["%.2e" % e for e in errs])
     del ws
     torch.cuda.empty_cache()
