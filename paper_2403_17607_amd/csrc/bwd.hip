@@ -240,10 +240,17 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void bwd_kernel(const BwdArgs 
       const int SI = (in_dim + 15) >> 4;
       const bool xv = (in_dim & 3) == 0;
       const rsrc_t xr = make_rsrc(a.dX + row0 * in_dim, vrows * in_dim * 4);
-      for (int s = 0; s < SI; ++s) {
-        u32x4 af[KBW];
+      // strip s + 1's fragments are requested while strip s computes
+      u32x4 af[KBW], an[KBW];
 #pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) af[kb] = a.packed0[(s * KBW + kb) * 64 + lane];
+      for (int kb = 0; kb < KBW; ++kb) an[kb] = a.packed0[kb * 64 + lane];
+      for (int s = 0; s < SI; ++s) {
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) af[kb] = an[kb];
+        if (s + 1 < SI) {
+#pragma unroll
+          for (int kb = 0; kb < KBW; ++kb) an[kb] = a.packed0[((s + 1) * KBW + kb) * 64 + lane];
+        }
         f32x4 acc[NT];
 #pragma unroll
         for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
