@@ -201,3 +201,31 @@ class Net:
         if want_deltas:
             out["D"] = self._deltas(D, M)
         return out
+
+
+# ------------------------------------------------------------- optimizer --
+# The paper leaves the optimizer out of the training step (section III-A);
+# applications need one.  These are the plain definitions, elementwise in
+# fp64 numpy: SGD, and Adam as in Kingma & Ba (2015), Algorithm 1, with the
+# bias corrections applied to the moment estimates.
+
+def sgd_step(w, g, lr):
+    """w - lr g."""
+    return np.asarray(w, np.float64) - lr * np.asarray(g, np.float64)
+
+
+def adam_step(w, m, v, g, lr, beta1, beta2, eps, t):
+    """One Adam step (t = 1, 2, ...): returns (w, m, v).
+    m <- beta1 m + (1 - beta1) g;  v <- beta2 v + (1 - beta2) g^2;
+    w <- w - lr * (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps)."""
+    w, m, v, g = (np.asarray(a, np.float64) for a in (w, m, v, g))
+    m = beta1 * m + (1.0 - beta1) * g
+    v = beta2 * v + (1.0 - beta2) * g * g
+    mhat = m / (1.0 - beta1 ** t)
+    vhat = v / (1.0 - beta2 ** t)
+    return w - lr * mhat / (np.sqrt(vhat) + eps), m, v
+
+
+def to_bf16(w):
+    """Round every value to bf16 (round to nearest, ties to even)."""
+    return np.vectorize(rne_bf16, otypes=[np.float64])(np.asarray(w, np.float64))

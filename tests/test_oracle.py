@@ -402,3 +402,48 @@ def test_invalid_arguments_rejected():
     with pytest.raises(ValueError):
         Net(width=4, depth=1, in_dim=4, out_dim=4, act=9).forward(
             np.zeros(32), np.zeros((1, 4)))
+
+
+# -------------------------------------------------------------- optimizer --
+
+def test_adam_first_step_closed_form():
+    """From zero moments the bias corrections cancel: the first step is
+    w - lr g / (|g| + eps)."""
+    g = RNG.uniform(-1, 1, 300)
+    w = RNG.uniform(-1, 1, 300)
+    lr, b1, b2, eps = 1e-2, 0.9, 0.999, 1e-8
+    w1, m1, v1 = oracle.adam_step(w, np.zeros(300), np.zeros(300), g, lr, b1, b2, eps, 1)
+    np.testing.assert_allclose(w1, w - lr * g / (np.abs(g) + eps), rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(m1, (1 - b1) * g, rtol=1e-15)
+    np.testing.assert_allclose(v1, (1 - b2) * g * g, rtol=1e-15)
+
+
+def test_adam_matches_torch_optim():
+    """Five steps against torch.optim.Adam (a library routine) in fp64."""
+    lr, b1, b2, eps = 3e-3, 0.8, 0.95, 1e-6
+    w0 = RNG.uniform(-1, 1, 257)
+    p = torch.nn.Parameter(torch.tensor(w0, dtype=torch.float64))
+    opt = torch.optim.Adam([p], lr=lr, betas=(b1, b2), eps=eps)
+    w, m, v = w0.copy(), np.zeros(257), np.zeros(257)
+    for t in range(1, 6):
+        g = RNG.uniform(-1, 1, 257)
+        p.grad = torch.tensor(g)
+        opt.step()
+        w, m, v = oracle.adam_step(w, m, v, g, lr, b1, b2, eps, t)
+    np.testing.assert_allclose(w, p.detach().numpy(), rtol=1e-12, atol=1e-15)
+
+
+def test_sgd_matches_torch_optim():
+    w0 = RNG.uniform(-1, 1, 100)
+    g = RNG.uniform(-1, 1, 100)
+    p = torch.nn.Parameter(torch.tensor(w0, dtype=torch.float64))
+    opt = torch.optim.SGD([p], lr=0.05)
+    p.grad = torch.tensor(g)
+    opt.step()
+    np.testing.assert_allclose(oracle.sgd_step(w0, g, 0.05), p.detach().numpy(), rtol=1e-13, atol=1e-16)
+
+
+def test_to_bf16_matches_torch():
+    w = RNG.uniform(-3, 3, 1000).astype(np.float32).astype(np.float64)
+    ref = torch.tensor(w, dtype=torch.float32).to(torch.bfloat16).to(torch.float64).numpy()
+    np.testing.assert_array_equal(oracle.to_bf16(w), ref)
