@@ -166,6 +166,32 @@ int mlp_train_step(const mlp_t* h, const void* packed, const uint16_t* X,
                    const float* T, uint16_t* Y, float* G, float* loss,
                    int64_t M, void* ws, void* stream);
 
+/* Optimizer step on fp32 master weights (NEXT-4; the paper leaves the
+ * optimizer out of its training step, section III-A).  One kernel updates
+ * every parameter, then writes the bf16 weights the fused kernels read
+ * (round to nearest even) and, when packed != NULL, re-packs them exactly as
+ * mlp_pack_weights does.  All buffers hold mlp_param_count(h) values in the
+ * weights' layout (the L matrices concatenated, each [fan_in][fan_out]).
+ *   master  fp32, updated in place; 4-byte aligned.
+ *   G       fp32 gradients (from mlp_train_step or mlp_backward).
+ *   W       bf16 output; 2-byte aligned.
+ *   packed  mlp_packed_bytes(h) bytes, 16-byte aligned, or NULL.
+ * SGD: master -= lr G. */
+int mlp_sgd_step(const mlp_t* h, float* master, const float* G, uint16_t* W,
+                 void* packed, float lr, void* stream);
+
+/* Adam (Kingma and Ba 2015, Algorithm 1), step t = 1, 2, ...:
+ *   m = beta1 m + (1 - beta1) G;  v = beta2 v + (1 - beta2) G^2;
+ *   master -= lr (m / (1 - beta1^t)) / (sqrt(v / (1 - beta2^t)) + eps).
+ *   m, v  fp32 moment buffers, updated in place (start from zeros).
+ * MLP_ERR_INVALID_ARG for t < 1, beta outside [0, 1), eps <= 0, a
+ * non-finite lr, or null or misaligned pointers.  Other arguments as for
+ * mlp_sgd_step. */
+int mlp_adam_step(const mlp_t* h, float* master, float* m, float* v,
+                  const float* G, uint16_t* W, void* packed, float lr,
+                  float beta1, float beta2, float eps, int64_t t,
+                  void* stream);
+
 /* Description of the last error on this thread ("" if none). */
 const char* mlp_last_error(void);
 

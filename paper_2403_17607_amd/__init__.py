@@ -61,6 +61,10 @@ _SIGNATURES = {
     "mlp_backward_dx": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_int64, _VP, _VP]),
     "mlp_train_step": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_int64,
                                       _VP, _VP]),
+    "mlp_sgd_step": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, ctypes.c_float, _VP]),
+    "mlp_adam_step": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_float,
+                                     ctypes.c_float, ctypes.c_float, ctypes.c_float,
+                                     ctypes.c_int64, _VP]),
     "mlp_last_error": (ctypes.c_char_p, []),
 }
 
@@ -200,6 +204,32 @@ class FusedMLP:
         _check(lib().mlp_backward(self._h, _ptr(packed), _ptr(X), _ptr(dY), _ptr(G), X.shape[0],
                                   _ptr(ws), _stream(X.device)))
         return G
+
+    def sgd_step(self, master: torch.Tensor, G: torch.Tensor, W: torch.Tensor,
+                 packed: torch.Tensor | None, lr: float) -> None:
+        """master -= lr G (fp32); W = bf16(master); re-packs into `packed`
+        when given."""
+        self._check_params(master, G, W)
+        _check(lib().mlp_sgd_step(self._h, _ptr(master), _ptr(G), _ptr(W), _ptr(packed), lr,
+                                  _stream(master.device)))
+
+    def adam_step(self, master: torch.Tensor, m: torch.Tensor, v: torch.Tensor, G: torch.Tensor,
+                  W: torch.Tensor, packed: torch.Tensor | None, lr: float,
+                  betas=(0.9, 0.999), eps: float = 1e-8, t: int = 1) -> None:
+        """One Adam step t (1, 2, ...) on fp32 master weights and moments;
+        W = bf16(master); re-packs into `packed` when given."""
+        self._check_params(master, G, W)
+        for b in (m, v):
+            assert b.dtype == torch.float32 and b.numel() == self.param_count() and b.is_contiguous()
+        _check(lib().mlp_adam_step(self._h, _ptr(master), _ptr(m), _ptr(v), _ptr(G), _ptr(W),
+                                   _ptr(packed), lr, betas[0], betas[1], eps, t,
+                                   _stream(master.device)))
+
+    def _check_params(self, master, G, W):
+        n = self.param_count()
+        assert master.dtype == torch.float32 and master.numel() == n and master.is_contiguous()
+        assert G.dtype == torch.float32 and G.numel() == n and G.is_contiguous()
+        assert W.dtype == torch.bfloat16 and W.numel() == n and W.is_contiguous()
 
     def backward_dx(self, packed: torch.Tensor, X: torch.Tensor, dY: torch.Tensor,
                     ws: torch.Tensor, G: torch.Tensor | None = None,

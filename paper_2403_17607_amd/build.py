@@ -18,7 +18,7 @@ ROOT = os.path.dirname(PKG)
 CSRC = os.path.join(PKG, "csrc")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libffmlp.so")
-SOURCES = ["api.hip", "fwd.hip", "bwd.hip", "wgrad.hip"]
+SOURCES = ["api.hip", "fwd.hip", "bwd.hip", "wgrad.hip", "optim.hip"]
 ARCH = "gfx950"
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"

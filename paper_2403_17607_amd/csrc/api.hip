@@ -3,6 +3,7 @@
 #include <hip/hip_runtime.h>
 
 #include <cstdarg>
+#include <cmath>
 #include <cstdio>
 #include <cstring>
 #include <mutex>
@@ -354,6 +355,65 @@ int mlp_pack_weights(const mlp_t* h, const uint16_t* W, void* packed, void* stre
   hipError_t e = launch_pack(a, static_cast<hipStream_t>(stream));
   if (e != hipSuccess) return hip_fail(e, "pack kernel launch");
   return MLP_OK;
+}
+
+
+namespace {
+
+int optim_step(const mlp_t* h, OptArgs a, void* packed, void* stream) {
+  if (!a.master || !a.G || !a.W) return fail(MLP_ERR_INVALID_ARG, "null master, G or W");
+  if (!aligned(a.master, 4) || !aligned(a.G, 4) || !aligned(a.W, 2) ||
+      (a.m && !aligned(a.m, 4)) || (a.v && !aligned(a.v, 4)) || (packed && !aligned(packed, 16)))
+    return fail(MLP_ERR_INVALID_ARG, "misaligned pointer (master, m, v, G: 4 bytes; W: 2; packed: 16)");
+  if (!std::isfinite(a.lr)) return fail(MLP_ERR_INVALID_ARG, "lr is not finite");
+  a.n = param_count(h);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  hipError_t e = launch_optim(a, s);
+  if (e != hipSuccess) return hip_fail(e, "optimizer kernel launch");
+  if (packed) return mlp_pack_weights(h, a.W, packed, stream);
+  return MLP_OK;
+}
+
+}  // namespace
+
+int mlp_sgd_step(const mlp_t* h, float* master, const float* G, uint16_t* W, void* packed,
+                 float lr, void* stream) {
+  g_err.clear();
+  if (int rc = check_handle(h)) return rc;
+  OptArgs a{};
+  a.master = master;
+  a.G = G;
+  a.W = W;
+  a.adam = 0;
+  a.lr = lr;
+  return optim_step(h, a, packed, stream);
+}
+
+int mlp_adam_step(const mlp_t* h, float* master, float* m, float* v, const float* G, uint16_t* W,
+                  void* packed, float lr, float beta1, float beta2, float eps, int64_t t,
+                  void* stream) {
+  g_err.clear();
+  if (int rc = check_handle(h)) return rc;
+  if (!m || !v) return fail(MLP_ERR_INVALID_ARG, "null Adam moment buffer");
+  if (t < 1) return fail(MLP_ERR_INVALID_ARG, "Adam step t = %lld < 1", (long long)t);
+  if (!(beta1 >= 0.f && beta1 < 1.f) || !(beta2 >= 0.f && beta2 < 1.f) || !(eps > 0.f))
+    return fail(MLP_ERR_INVALID_ARG, "need 0 <= beta1, beta2 < 1 and eps > 0");
+  OptArgs a{};
+  a.master = master;
+  a.m = m;
+  a.v = v;
+  a.G = G;
+  a.W = W;
+  a.adam = 1;
+  a.lr = lr;
+  a.beta1 = beta1;
+  a.beta2 = beta2;
+  a.eps = eps;
+  const double bc1 = 1.0 - std::pow((double)beta1, (double)t);
+  const double bc2 = 1.0 - std::pow((double)beta2, (double)t);
+  a.step_size = (float)((double)lr / bc1);
+  a.inv_sqrt_bc2 = (float)(1.0 / std::sqrt(bc2));
+  return optim_step(h, a, packed, stream);
 }
 
 size_t mlp_workspace_bytes(const mlp_t* h, int64_t M, int mode) {

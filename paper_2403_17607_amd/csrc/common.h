@@ -165,6 +165,19 @@ struct PackArgs {
   int64_t total;      // bf16 elements of the packed buffer
 };
 
+struct OptArgs {
+  float* master;      // fp32 master weights, updated in place
+  float* m;           // Adam first moments (null for SGD)
+  float* v;           // Adam second moments (null for SGD)
+  const float* G;     // gradients, the weights' layout
+  uint16_t* W;        // bf16 copy of the updated master weights
+  int64_t n;          // parameter count
+  int adam;
+  float lr, beta1, beta2, eps;
+  float step_size;     // lr / (1 - beta1^t)
+  float inv_sqrt_bc2;  // 1 / sqrt(1 - beta2^t)
+};
+
 // Host-side launchers (one per translation unit).  They return a HIP error.
 hipError_t launch_forward(int width, int act, int mode, const FwdArgs& a,
                           hipStream_t s, int* grid_out);
@@ -173,6 +186,7 @@ hipError_t launch_backward(int width, int act, int seeded, const BwdArgs& a,
 hipError_t launch_wgrad(int width, const WgradArgs& a, hipStream_t s);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
+hipError_t launch_optim(const OptArgs& a, hipStream_t s);
 
 // Forward kernel modes.
 enum { FWD_INFER = 0, FWD_STASH = 1, FWD_TRAIN = 2 };

@@ -21,6 +21,7 @@ def declared_functions():
 def test_header_declares_the_boundary():
     names = declared_functions()
     for required in ["mlp_create", "mlp_forward", "mlp_backward", "mlp_backward_dx", "mlp_train_step",
+                     "mlp_sgd_step", "mlp_adam_step",
                      "mlp_pack_weights", "mlp_workspace_bytes", "mlp_destroy"]:
         assert required in names
 
@@ -115,4 +116,18 @@ def test_null_and_bad_arguments_fail_before_any_launch(ffmlp):
         ffmlp.MLP_ERR_INVALID_ARG
     assert L.mlp_pack_weights(h, None, fake, None) == ffmlp.MLP_ERR_INVALID_ARG
     assert L.mlp_set_output_activation(h, 9) == ffmlp.MLP_ERR_UNSUPPORTED
+    assert L.mlp_backward_dx(h, fake, fake, fake, fake, ctypes.c_void_p(0x1004), 10, fake, None) == \
+        ffmlp.MLP_ERR_INVALID_ARG  # misaligned dX
+    # optimizer: every check happens before the launch
+    inv = ffmlp.MLP_ERR_INVALID_ARG
+    assert L.mlp_sgd_step(h, None, fake, fake, None, 0.1, None) == inv
+    assert L.mlp_sgd_step(h, fake, fake, fake, None, float("nan"), None) == inv
+    assert L.mlp_sgd_step(h, ctypes.c_void_p(0x1002), fake, fake, None, 0.1, None) == inv
+    assert L.mlp_adam_step(h, fake, fake, fake, fake, fake, None, 1e-3, 0.9, 0.999, 1e-8, 0, None) == inv
+    assert "t = 0" in ffmlp.last_error()
+    assert L.mlp_adam_step(h, fake, fake, fake, fake, fake, None, 1e-3, 1.0, 0.999, 1e-8, 1, None) == inv
+    assert L.mlp_adam_step(h, fake, fake, fake, fake, fake, None, 1e-3, 0.9, 0.999, 0.0, 1, None) == inv
+    assert L.mlp_adam_step(h, fake, None, fake, fake, fake, None, 1e-3, 0.9, 0.999, 1e-8, 1, None) == inv
+    assert L.mlp_adam_step(h, fake, fake, fake, fake, fake, ctypes.c_void_p(0x1008), 1e-3, 0.9,
+                           0.999, 1e-8, 1, None) == inv  # misaligned packed
     L.mlp_destroy(None)  # ignored

@@ -266,6 +266,75 @@ def test_chained_nets_nerf_like(ffmlp, gpu):
     log("  density grad errs", ["%.2e" % e for e in check_grads(f64(Gd), Gd_ref, odens)])
 
 
+# ---------------------------------------------------- optimizer (NEXT-4) --
+
+def test_optimizer_steps_match_oracle(ffmlp, gpu):
+    """Three Adam steps, then one SGD step, on fp32 master weights: master
+    weights and moments against the fp64 definitions, W bitwise the bf16
+    rounding of the GPU's own master weights (and of the oracle's on all
+    but boundary cases), and the re-packed buffer equal to a fresh pack."""
+    import oracle
+    net = ffmlp.FusedMLP(64, 3, 40, 10, "relu")
+    n = net.param_count()
+    W0 = datagen.xavier_weights(8, 64, 3, 40, 10)
+    Gs = [datagen.uniform(8 + t, datagen.STREAM_AUX, (n,)) * 1e-2 for t in range(4)]
+    master = W0.float().to(gpu)
+    m = torch.zeros(n, dtype=torch.float32, device=gpu)
+    v = torch.zeros_like(m)
+    W = torch.empty(n, dtype=torch.bfloat16, device=gpu)
+    packed = torch.empty(net.packed_bytes(), dtype=torch.uint8, device=gpu)
+    wo, mo, vo = f64(W0), np.zeros(n), np.zeros(n)
+    lr, b1, b2, eps = 1e-2, 0.9, 0.99, 1e-8
+    for t in range(1, 4):
+        net.adam_step(master, m, v, Gs[t - 1].to(gpu), W, packed, lr, (b1, b2), eps, t)
+        wo, mo, vo = oracle.adam_step(wo, mo, vo, f64(Gs[t - 1]), lr, b1, b2, eps, t)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(f64(master), wo, rtol=0, atol=1e-6)
+    # fp32 against fp64: a few fp32 ulps of the moments' scale (m can cancel
+    # to near zero, so the bound is absolute)
+    np.testing.assert_allclose(f64(m), mo, rtol=0, atol=1e-6 * np.abs(mo).max())
+    np.testing.assert_allclose(f64(v), vo, rtol=0, atol=1e-6 * np.abs(vo).max())
+    assert np.array_equal(f64(W), oracle.to_bf16(f64(master)))
+    assert np.mean(f64(W) == oracle.to_bf16(wo)) > 0.999
+    assert torch.equal(packed, net.pack(W))
+    net.sgd_step(master, Gs[3].to(gpu), W, None, 0.5)
+    torch.cuda.synchronize()
+    np.testing.assert_allclose(f64(master), oracle.sgd_step(wo, f64(Gs[3]), 0.5), rtol=0, atol=2e-6)
+    assert np.array_equal(f64(W), oracle.to_bf16(f64(master)))
+
+
+def test_adam_training_loop_matches_oracle(ffmlp, gpu):
+    """Five training steps (train step, then Adam with re-packing) on the
+    GPU against the same loop on the oracle: losses agree and fall."""
+    import oracle
+    width, depth, in_dim, out_dim, M = 32, 2, 32, 8, 2048
+    W0, X, T = inputs(9, width, depth, in_dim, out_dim, M)
+    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, "relu")
+    onet = oracle_net(width, depth, in_dim, out_dim, "relu")
+    n = net.param_count()
+    master = W0.float().to(gpu)
+    m = torch.zeros(n, dtype=torch.float32, device=gpu)
+    v = torch.zeros_like(m)
+    W = W0.to(gpu).clone()
+    packed = net.pack(W)
+    ws = net.workspace(M, gpu)
+    Xd, Td = X.to(gpu), T.to(gpu)
+    wo, mo, vo, Wb = f64(W0), np.zeros(n), np.zeros(n), f64(W0)
+    lr, b1, b2, eps = 2e-2, 0.9, 0.999, 1e-8
+    gl, ol = [], []
+    for t in range(1, 6):
+        G, loss = net.train_step(packed, Xd, Td, ws)
+        net.adam_step(master, m, v, G, W, packed, lr, (b1, b2), eps, t)
+        gl.append(loss.item())
+        r = onet.train_step(Wb, X, T)
+        ol.append(r["loss"])
+        wo, mo, vo = oracle.adam_step(wo, mo, vo, r["G"], lr, b1, b2, eps, t)
+        Wb = oracle.to_bf16(wo)
+    log("  losses gpu", ["%.6f" % x for x in gl], "oracle", ["%.6f" % x for x in ol])
+    np.testing.assert_allclose(gl, ol, rtol=1e-2)
+    assert gl[-1] < gl[0] and ol[-1] < ol[0]
+
+
 # ------------------------------------------- full sizes, sampled rows only --
 
 def sampled_rows(M, n, seed):
