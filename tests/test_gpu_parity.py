@@ -266,6 +266,55 @@ def test_chained_nets_nerf_like(ffmlp, gpu):
     log("  density grad errs", ["%.2e" % e for e in check_grads(f64(Gd), Gd_ref, odens)])
 
 
+# ------------------------------------------------ HIP graph capture (NEXT-3) --
+
+def test_graph_capture_replays_bitwise(ffmlp, gpu):
+    """The library neither allocates nor synchronizes, so a forward pass, a
+    training step and an Adam step can be captured in one HIP graph (what a
+    small-batch loop needs to shed launch overhead).  Every replay, with
+    other work and synchronizations between replays, equals the eager
+    results bit for bit."""
+    width, depth, in_dim, out_dim, M = 64, 4, 64, 16, 4096
+    W, X, T = inputs(12, width, depth, in_dim, out_dim, M)
+    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, "relu")
+    n = net.param_count()
+    Xd, Td = X.to(gpu), T.to(gpu)
+    ws = net.workspace(M, gpu)
+
+    def step(packed, master, m, v, Wb, G, loss, Yt, Yf):
+        net.train_step(packed, Xd, Td, ws, G=G, loss=loss, Y=Yt)
+        net.forward(packed, Xd, Y=Yf)
+        net.adam_step(master, m, v, G, Wb, packed, 1e-3, (0.9, 0.999), 1e-8, 1)
+
+    def state():
+        Wb = W.to(gpu).clone()
+        return dict(packed=net.pack(Wb), master=Wb.float(), m=torch.zeros(n, device=gpu),
+                    v=torch.zeros(n, device=gpu), Wb=Wb,
+                    G=torch.empty(n, device=gpu), loss=torch.empty(1, device=gpu),
+                    Yt=torch.empty(M, out_dim, dtype=torch.bfloat16, device=gpu),
+                    Yf=torch.empty(M, out_dim, dtype=torch.bfloat16, device=gpu))
+
+    eager = state()
+    step(**eager)  # also fills the launch caches before capture
+    torch.cuda.synchronize()
+    cap = state()
+    graph = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(graph):
+        step(**cap)
+    for rep in range(3):
+        fresh = state()  # reset the captured buffers' inputs
+        for k in ("packed", "master", "m", "v", "Wb"):
+            cap[k].copy_(fresh[k])
+        torch.cuda.synchronize()
+        graph.replay()
+        other = state()
+        step(**other)  # eager work between replays
+        torch.cuda.synchronize()
+        for k in eager:
+            assert torch.equal(cap[k], eager[k]), (rep, k)
+            assert torch.equal(other[k], eager[k]), (rep, k)
+
+
 # ---------------------------------------------------- optimizer (NEXT-4) --
 
 def test_optimizer_steps_match_oracle(ffmlp, gpu):
