@@ -396,6 +396,7 @@ def sampled_rows(M, n, seed):
     (64, 4, 64, 16, (1 << 20) + 37),  # ragged tail
     (32, 4, 32, 16, 1 << 20),
     (16, 4, 16, 16, 1 << 22),         # width sweep at 2^22
+    (128, 4, 128, 16, 1 << 22),       # the largest sweep batch at width 128
     (128, 16, 128, 128, 1 << 20),     # depth/width stress: weights stream through LDS
     (128, 3, 128, 16, (1 << 20) + 100),  # even matrix count, ragged tail
     (64, 5, 64, 16, 1 << 20),         # even matrix count at width 64
