@@ -106,9 +106,19 @@ def cpu_baseline(width, depth, in_dim, out_dim, act, out_act, target_s=12.0):
         m = int(min(max(m * target_s / max(dt, 1e-3), 2 * m), 1 << 22))
         dt = run(m)
     threads = int(os.environ.get("OMP_NUM_THREADS", "0")) or os.cpu_count()
+    # the same on one core, on a smaller sample (about 3 s)
+    net1 = oracle.Net(width, depth, in_dim, out_dim, acts[act], acts[out_act], threads=1)
+    m1 = max(256, int(m / dt / threads * 3.0))
+    X1 = datagen.inputs_uniform(3, m1, in_dim)
+    T1 = datagen.targets_uniform(3, m1, out_dim)
+    t0 = time.perf_counter()
+    net1.forward(W, X1)
+    net1.train_step(W, X1, T1)
+    dt1 = time.perf_counter() - t0
     return {"value": m / dt, "unit": "samples/s", "cores": threads, "kind": "oracle",
             "sample": f"{m} rows of the same net and input recipe, inference forward + training "
-                      f"step, fp64, {dt:.1f} s"}
+                      f"step, fp64, {dt:.1f} s",
+            "value_1core": m1 / dt1, "sample_1core": f"{m1} rows, {dt1:.1f} s"}
 
 
 def main():
