@@ -47,9 +47,12 @@ __device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], const u32x
 // the register allocation of one loop does not constrain another and no
 // loop carries the other's branches (whose joins force conservative waits
 // on LDS loads).
-template <int W, int ACT, int MODE, int FU, bool RES>
+// SMALL: one 16-row block per wave (inference on batches that give the
+// usual tiles fewer than two per compute unit, widths up to 64): four
+// times as many workgroups, so more waves share each CU's latency.
+template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false>
 __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs a) {
-  constexpr int NT = TileCfg<W>::NT, NW = TileCfg<W>::NW;
+  constexpr int NT = SMALL ? 1 : TileCfg<W>::NT, NW = TileCfg<W>::NW;
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
   extern __shared__ u32x4 smem[];
   __shared__ float red[NW];
@@ -496,6 +499,15 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
   if constexpr (MODE == FWD_INFER && W >= 64) {
     if (a.resident && a.L >= 2 && SO == 1 && (a.in_dim % 8) == 0)
       kern = (a.L & 1) ? fwd_kernel<W, ACT, MODE, 1, true> : fwd_kernel<W, ACT, MODE, 2, true>;
+  }
+  if constexpr (MODE == FWD_INFER && W <= 64) {
+    // Small batches: fewer than two of the usual row tiles per CU (widths
+    // up to 64, whose weights leave LDS for several workgroups per CU).
+    if (a.ntiles <= 2 * di.cus && a.resident) {
+      kern = fwd_kernel<W, ACT, MODE, 0, true, true>;
+      const int64_t rows = (int64_t)TileCfg<W>::NW * 16;
+      a.ntiles = (int)((a.M + rows - 1) / rows);
+    }
   }
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), NTH, lds, &occ);
