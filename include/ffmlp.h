@@ -17,7 +17,8 @@
  * L = depth + 1 weight matrices: in_dim x width, (depth - 1) times
  * width x width, width x out_dim (for depth = 0: one in_dim x out_dim
  * matrix).  width is 16, 32, 64 or 128 (section I); 1 <= in_dim, out_dim
- * <= width.  Smaller input and output widths are reduced to the square case
+ * <= width; 0 <= depth <= MLP_MAX_DEPTH (the weight-gradient launch has one
+ * grid row per matrix, and a grid dimension holds at most 65535).  Smaller input and output widths are reduced to the square case
  * by zero padding inside the library (section III-A).
  *
  * Precision.  All matrix products take bf16 operands and accumulate in fp32
@@ -70,10 +71,12 @@ enum {
 
 enum { MLP_MODE_INFER = 0, MLP_MODE_TRAIN = 1 };
 
+enum { MLP_MAX_DEPTH = 65534 };
+
 /* Create a handle (host memory only).  `activation` applies to the hidden
  * layers; the output activation defaults to linear.  Returns
  * MLP_ERR_UNSUPPORTED for a width outside {16, 32, 64, 128} or an unknown
- * activation, MLP_ERR_INVALID_ARG for depth < 0, in_dim or out_dim outside
+ * activation, MLP_ERR_INVALID_ARG for depth outside [0, MLP_MAX_DEPTH], in_dim or out_dim outside
  * [1, width], or out == NULL. */
 int mlp_create(int width, int depth, int in_dim, int out_dim, int activation,
                mlp_t** out);

@@ -297,7 +297,8 @@ int mlp_create(int width, int depth, int in_dim, int out_dim, int activation, ml
   if (width != 16 && width != 32 && width != 64 && width != 128)
     return fail(MLP_ERR_UNSUPPORTED, "width %d is not one of 16, 32, 64, 128", width);
   if (!valid_act(activation)) return fail(MLP_ERR_UNSUPPORTED, "unknown activation %d", activation);
-  if (depth < 0) return fail(MLP_ERR_INVALID_ARG, "depth %d < 0", depth);
+  if (depth < 0 || depth > MLP_MAX_DEPTH)
+    return fail(MLP_ERR_INVALID_ARG, "depth %d outside [0, %d]", depth, (int)MLP_MAX_DEPTH);
   if (in_dim < 1 || in_dim > width)
     return fail(MLP_ERR_INVALID_ARG, "in_dim %d outside [1, %d]", in_dim, width);
   if (out_dim < 1 || out_dim > width)

@@ -307,32 +307,35 @@ __global__ __launch_bounds__(256) void pack_kernel(const PackArgs a) {
   const int Wd = a.width, L = a.L;
   auto fan_in = [&](int l) { return l == 0 ? a.in_dim : Wd; };
   auto fan_out = [&](int l) { return l == L - 1 ? a.out_dim : Wd; };
-  // locate the layer and orientation of element e0: forward layers
+  // Locate the layer and orientation of element e0: forward layers
   // 0 .. L-1, backward layers 1 .. L-1, then backward layer 0 (read only
-  // by the input-gradient step)
+  // by the input-gradient step).  A segment holds strips(rows) fragments of
+  // 512 elements per k-block, rows being the fan_out (forward) or fan_in
+  // (backward) of its layer, so every hidden segment has the same size and
+  // the position follows in closed form, whatever the depth.
+  const int64_t per = (int64_t)((Wd + 31) / 32) * 512;  // one strip
+  const int64_t nW = per * ((Wd + 15) / 16);
+  const int64_t nO = per * ((a.out_dim + 15) / 16);
+  const int64_t nH = (int64_t)(L - 1) * nW;  // L - 1 segments of nW
   int64_t e = e0;
-  int dir = 0, l = 0;
-  for (int seg = 0;; ++seg) {
-    if (seg < L) {
-      dir = 0;
-      l = seg;
-    } else if (seg < 2 * L - 1) {
-      dir = 1;
-      l = seg - L + 1;
-    } else if (seg == 2 * L - 1) {
-      dir = 1;
-      l = 0;
-    } else {
-      return;  // not reached: e0 < total
-    }
-    const int fi = fan_in(l), fo = fan_out(l);
-    const int rows = dir == 0 ? fo : fi;
-    const int64_t n = (int64_t)((rows + 15) / 16) * ((Wd + 31) / 32) * 512;
-    if (e < n) break;
-    e -= n;
+  int dir, l;
+  if (e < nH) {
+    dir = 0;
+    l = (int)(e / nW);
+    e -= (int64_t)l * nW;
+  } else if ((e -= nH) < nO) {
+    dir = 0;
+    l = L - 1;
+  } else if ((e -= nO) < nH) {
+    dir = 1;
+    l = 1 + (int)(e / nW);
+    e -= (int64_t)(l - 1) * nW;
+  } else {
+    e -= nH;  // < strips(in_dim) strips: e0 < total
+    dir = 1;
+    l = 0;
   }
-  int64_t woff = 0;
-  for (int k = 0; k < l; ++k) woff += (int64_t)fan_in(k) * fan_out(k);
+  const int64_t woff = l == 0 ? 0 : (int64_t)a.in_dim * Wd + (int64_t)(l - 1) * Wd * Wd;
   const int fi = fan_in(l), fo = fan_out(l);
   const int kblocks = (Wd + 31) / 32;  // every layer is padded to the width's k-blocks
   const int slot = (int)(e & 7), lane = (int)((e >> 3) & 63);

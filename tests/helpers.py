@@ -4,8 +4,8 @@ oracle's view of a net, and the two error measures with their bounds.
 Bounds (per output and per weight-gradient matrix), for a net with L
 weight matrices:
   outputs    max_i |Y_i - Yref_i| / max(|Yref_i|, rms(Yref)) <= 2e-2 s(L)
-             ||Y - Yref||_F / ||Yref||_F <= 2e-3
-             99.9th percentile of the per-element error above <= 2e-2
+             ||Y - Yref||_F / ||Yref||_F <= 2e-3 sqrt(s(L))
+             99.9th percentile of the per-element error above <= 2e-2 sqrt(s(L))
   gradients  ||G_l - Gref_l||_F / ||Gref_l||_F <= 1e-2 s(L)
 with s(L) = max(1, L / 5).  The GPU rounds to bf16 at the same points as the
 oracle; what differs is the fp32 (GPU) versus fp64 (oracle) accumulation,
@@ -15,9 +15,14 @@ The number of rounding stages grows with L, so the worst-element bounds
 (2e-2 and 1e-2, stated for nets of up to 5 matrices) scale with L / 5; a
 CPU model with fp32 sums and the same rounding points departs from the
 oracle by as much (3.5e-2 on outputs, 1.5e-2 on gradients at L = 17).  The
-aggregate bounds do not scale.
+aggregate bounds scale with sqrt(s(L)), as flips of independent stages add
+up like a random walk: the same model on deep sine nets departs by
+Frobenius 3.8e-3 and 99.9th percentile 4.0e-2 at L = 61 (fixed bounds of
+2e-3 and 2e-2 cannot hold at every depth).
 """
 from __future__ import annotations
+
+import math
 
 import numpy as np
 import torch
@@ -77,8 +82,11 @@ def check_outputs(Y, Yref, n_mats: int) -> dict:
     fro = float(np.linalg.norm(Y - Yref) / nref) if nref > 0 else float(np.linalg.norm(Y))
     res = {"max": float(e.max()), "p999": float(np.quantile(e, 0.999)), "fro": fro}
     assert res["max"] <= OUT_TOL * depth_scale(n_mats), res
-    assert res["p999"] <= OUT_P999_TOL, res
-    assert res["fro"] <= OUT_FRO_TOL, res
+    # Rounding flips of independent stages add up like a random walk, so the
+    # aggregate bounds grow with the square root of the depth factor.
+    agg = math.sqrt(depth_scale(n_mats))
+    assert res["p999"] <= OUT_P999_TOL * agg, res
+    assert res["fro"] <= OUT_FRO_TOL * agg, res
     return res
 
 

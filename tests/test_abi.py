@@ -60,6 +60,12 @@ def test_shapes_and_offsets(ffmlp, width):
     assert net.packed_bytes() == (fwd + bwd) * 1024
 
 
+def test_deepest_net_is_accepted(ffmlp):
+    net = ffmlp.FusedMLP(16, 65534, 16, 16, "relu")
+    assert net.param_count() == 65535 * 256
+    assert net.layer_shape(65534) == (16, 16, 65534 * 256)
+
+
 def test_depth0_single_matrix(ffmlp):
     net = ffmlp.FusedMLP(32, 0, 20, 7, "sine")
     assert net.layer_shape(0) == (20, 7, 0)
@@ -88,6 +94,7 @@ def test_workspace_sizes(ffmlp):
     ((48, 2, 8, 8, 1), -2),     # width not supported
     ((64, 2, 8, 8, 7), -2),     # unknown activation
     ((64, -1, 8, 8, 1), -1),    # negative depth
+    ((64, 65535, 8, 8, 1), -1), # deeper than one grid dimension holds
     ((64, 2, 0, 8, 1), -1),     # in_dim < 1
     ((64, 2, 65, 8, 1), -1),    # in_dim > width
     ((64, 2, 8, 65, 1), -1),    # out_dim > width

@@ -83,6 +83,13 @@ def test_depths(ffmlp, gpu, width, depth):
     run_case(ffmlp, gpu, width, depth, width, width, 1000, seed=5)
 
 
+@pytest.mark.parametrize("width,depth,in_dim,out_dim", [(16, 100, 16, 16), (32, 60, 5, 9)])
+def test_deep_nets(ffmlp, gpu, width, depth, in_dim, out_dim):
+    """Deep sine nets (the weights stream through LDS layer by layer, and the
+    packed buffer has hundreds of segments, located in closed form)."""
+    run_case(ffmlp, gpu, width, depth, in_dim, out_dim, 700, act="sine", seed=23)
+
+
 @pytest.mark.parametrize("width,in_dim,out_dim", [(64, 1, 1), (64, 3, 3), (64, 16, 16),
                                                   (64, 8, 1), (64, 5, 64), (128, 127, 33),
                                                   (16, 1, 16), (32, 17, 31), (128, 40, 100)])
