@@ -64,31 +64,25 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   // per-unit byte offsets do not depend on the chunk and are computed once.
   //
   // Tile-image tensor with F features: unit v covers rows 16 tl + 2 ip,
-  // +1 and features 16 s + 4 g + 0..3.  Consecutive lanes take consecutive
-  // ip then tl, so a wave's transposed LDS writes hit distinct banks while
-  // every 8 lanes still read one contiguous 128-byte line.
+  // +1 and features 16 s + 4 g + 0..3, and sits at byte 16 v of the chunk,
+  // so a wave reads 1 KiB in one piece.  The transposed LDS writes of each
+  // half-wave (ip and g vary) still hit 32 distinct banks.
   struct TileUnit {
     int tl, s, g, ip;
   };
   auto tile_unit = [&](int v, int S) {
-    const int ip = v & 7, tla = (v >> 3) & 3, rest2 = v >> 5;
-    const int g = rest2 & 3, rest3 = rest2 >> 2;
-    return TileUnit{(rest3 / S) * 4 + tla, rest3 % S, g, ip};
+    const int ip = v & 7, g = (v >> 3) & 3, rest = v >> 5;
+    return TileUnit{rest / S, rest % S, g, ip};
   };
   // Byte offset of unit v inside the chunk (past the chunk when v >= U).
-  auto tile_voff = [&](int v, int S) {
-    const TileUnit t = tile_unit(v, S);
-    return (uint32_t)((((t.tl * S + t.s) * 4 + t.g) * 8 + t.ip) * 16);
-  };
+  auto tile_voff = [&](int v) { return (uint32_t)(v * 16); };
   const bool xmode = (l == 0);
   uint32_t voa[UPT], vod[UPT];
   {
-    const int SA = W / 16, SD = dF / 16;
 #pragma unroll
     for (int k = 0; k < UPT; ++k) {
-      const int v = k * 256 + tid;
-      vod[k] = tile_voff(v, SD);  // >= the chunk size when v is past it
-      voa[k] = tile_voff(v, SA);
+      vod[k] = tile_voff(k * 256 + tid);  // >= the chunk size when past it
+      voa[k] = vod[k];
     }
     if (xmode) {
       // X (row-major, in_dim a multiple of 8): unit pair q covers rows
