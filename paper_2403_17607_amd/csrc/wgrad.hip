@@ -259,8 +259,19 @@ __global__ __launch_bounds__(256) void reduce1_kernel(const ReduceArgs a) {
   if (e >= a.params) return;
   const int p0 = (int)((int64_t)a.P * y / kReduceSlices);
   const int p1 = (int)((int64_t)a.P * (y + 1) / kReduceSlices);
+  // Loads go out eight at a time, then are added in order: the same sum,
+  // without one memory latency per partial.
+  const float* src = a.partial + e;
   float s = 0.f;
-  for (int p = p0; p < p1; ++p) s += a.partial[(int64_t)p * a.params + e];
+  int p = p0;
+  for (; p + 8 <= p1; p += 8) {
+    float v[8];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) v[k] = src[(int64_t)(p + k) * a.params];
+#pragma unroll
+    for (int k = 0; k < 8; ++k) s += v[k];
+  }
+  for (; p < p1; ++p) s += src[(int64_t)p * a.params];
   a.mid[(int64_t)y * a.params + e] = s;
 }
 
