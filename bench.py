@@ -134,6 +134,10 @@ def main():
     ap.add_argument("--act", default="relu")
     ap.add_argument("--out-act", default="linear")
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle timing")
+    ap.add_argument("--inputs", choices=["default", "cold", "hot"], default="default",
+                    help="default: X alternates between two buffers; cold: X and T rotate "
+                         "over at least 512 MiB of buffers (beyond the 256 MiB last-level "
+                         "cache); hot: one X and T buffer every step")
     args = ap.parse_args()
     if args.gpus != 1:
         print("bench.py runs on one GPU only: this build has no multi-GPU path "
@@ -151,10 +155,17 @@ def main():
     dev = torch.device("cuda:0")
     net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, args.act, args.out_act)
     W = datagen.xavier_weights(2, width, depth, in_dim, out_dim, device=dev)
-    # two input buffers, alternated, so inference does not run out of the
-    # 256 MiB last-level cache
-    Xs = [datagen.inputs_uniform(2 + i, M, in_dim, device=dev) for i in range(2)]
-    T = datagen.targets_uniform(2, M, out_dim, device=dev)
+    # Input buffers used in turn.  By default two, so inference at large
+    # batches does not run out of the 256 MiB last-level cache; "cold"
+    # rotates X and T over at least 512 MiB whatever the batch, "hot" reuses
+    # one of each.
+    if args.inputs == "cold":
+        nbuf = max(2, -(-(512 << 20) // max(1, M * (2 * in_dim + 4 * out_dim))))
+    else:
+        nbuf = 1 if args.inputs == "hot" else 2
+    Xs = [datagen.inputs_uniform(2 + i, M, in_dim, device=dev) for i in range(nbuf)]
+    Ts = [datagen.targets_uniform(2 + i, M, out_dim, device=dev)
+          for i in range(nbuf if args.inputs == "cold" else 1)]
     packed = net.pack(W)
     ws = net.workspace(M, dev)
     Y = torch.empty(M, out_dim, dtype=torch.bfloat16, device=dev)
@@ -171,10 +182,11 @@ def main():
         net.pack(W, out=packed)
         if events:
             events[1].record(stream)
-        net.forward(packed, Xs[i % 2], Y=Y)
+        x = Xs[i % len(Xs)]
+        net.forward(packed, x, Y=Y)
         if events:
             events[2].record(stream)
-        net.train_step(packed, Xs[i % 2], T, ws, G=G, loss=loss)
+        net.train_step(packed, x, Ts[i % len(Ts)], ws, G=G, loss=loss)
         if events:
             events[3].record(stream)
 
@@ -222,7 +234,10 @@ def main():
                                f"out {out_dim}, {args.act} hidden, {args.out_act} output, "
                                f"batch {M}: weight pack + inference + training step",
                    "width": width, "depth": depth, "in_dim": in_dim, "out_dim": out_dim,
-                   "batch": M, "activation": args.act, "output_activation": args.out_act},
+                   "batch": M, "activation": args.act, "output_activation": args.out_act,
+                   "inputs": {"default": "X alternates between 2 buffers",
+                              "cold": f"X and T rotate over {nbuf} buffers (>= 512 MiB)",
+                              "hot": "one X and T buffer"}[args.inputs]},
         "infer": {"ms": t_inf, "samples_per_s": M / (t_inf * 1e-3), "tflops": inf_tflops,
                   "pct_bf16_peak": 100 * inf_tflops / PEAK_BF16_TFLOPS,
                   "hbm_gbs_algorithmic": bytes_inf / (t_inf * 1e-3) / 1e9},
