@@ -126,21 +126,26 @@ __device__ __forceinline__ u32x4 bload128(rsrc_t r, uint32_t voff, uint32_t soff
 __device__ __forceinline__ uint32_t bload32(rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
 }
-// Stores are non-temporal (cache policy nt): everything the forward and
-// backward kernels store (outputs, the activation and delta stash, masks,
-// dX) is read at most once, by a later kernel, so keeping it in L2 and the
-// last-level cache would only evict lines that are still in use.  Measured
-// on the training step: 4.7% faster at width 128 and 9% at width 64
-// (2^20 rows).
+// Stores are non-temporal (cache policy nt) by default: everything the
+// forward and backward kernels store (outputs, the activation and delta
+// stash, masks, dX) is read at most once, by a later kernel, so keeping it
+// in L2 and the last-level cache would only evict lines that are still in
+// use.  Measured on the training step: 4.7% faster at width 128 and 9% at
+// width 64 (2^20 rows).  NT = false gives the default policy, whose stores
+// are acknowledged sooner: a kernel that waits for all its stores at every
+// layer (streamed weights) and gains nothing later uses it for inference.
 constexpr int kStoreNT = 2;  // the nt bit of the buffer instructions' cache policy
+template <bool NT = true>
 __device__ __forceinline__ void bstore32(uint32_t v, rsrc_t r, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, kStoreNT);
+  __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, NT ? kStoreNT : 0);
 }
+template <bool NT = true>
 __device__ __forceinline__ void bstore64(u32x2 v, rsrc_t r, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, kStoreNT);
+  __builtin_amdgcn_raw_buffer_store_b64(v, r, voff, soff, NT ? kStoreNT : 0);
 }
+template <bool NT = true>
 __device__ __forceinline__ void bstore128(u32x4 v, rsrc_t r, uint32_t voff, uint32_t soff) {
-  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, kStoreNT);
+  __builtin_amdgcn_raw_buffer_store_b128(v, r, voff, soff, NT ? kStoreNT : 0);
 }
 
 // Asynchronous copy of nfrag 1 KiB fragments from global memory into LDS

@@ -68,6 +68,10 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
   const bool yvec = (out_dim & 3) == 0;
   const int out_act = a.out_act;
   constexpr bool resident = RES;
+  // Non-temporal stores, except for inference with streamed weights: there
+  // every layer ends by waiting for all outstanding memory operations, the
+  // output stores included, and nothing reads Y soon after.
+  constexpr bool NTS = RES || MODE != FWD_INFER;
   const int G = gridDim.x;
   auto layer_off = [&](int l) -> uint32_t {
     return l == 0 ? 0u : a.lay0_frags + (uint32_t)(l - 1) * a.layH_frags;
@@ -261,11 +265,11 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
           }
           if constexpr (MODE != FWD_INFER) {
             const uint32_t so = (uint32_t)((n * SW + s) * 512);
-            bstore64(u32x2{p0, p1}, sa, lane * 8, so);
+            bstore64<NTS>(u32x2{p0, p1}, sa, lane * 8, so);
             if constexpr (ACT == ACT_SINE) {
               const uint32_t c0 = pack_bf16x2(__cosf(acc[n][0]), __cosf(acc[n][1]));
               const uint32_t c1 = pack_bf16x2(__cosf(acc[n][2]), __cosf(acc[n][3]));
-              bstore64(u32x2{c0, c1}, ss, lane * 8, so);
+              bstore64<NTS>(u32x2{c0, c1}, ss, lane * 8, so);
             }
           }
         }
@@ -276,7 +280,7 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
         const rsrc_t mr = make_rsrc(a.reluMask + ((size_t)l * (a.M16 / 16) + tb0) * 64,
                                     a.reluMask ? (int64_t)vblk * 256 : 0);
 #pragma unroll
-        for (int n = 0; n < NT; ++n) bstore32(mk[n], mr, lane * 4, (uint32_t)(n * 256));
+        for (int n = 0; n < NT; ++n) bstore32<NTS>(mk[n], mr, lane * 4, (uint32_t)(n * 256));
       }
       if (!resident) {
         drain_and_sync();  // next layer staged; this buffer free again
@@ -304,7 +308,7 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
         const uint32_t y0 = pack_bf16x2(y[0], y[1]), y1 = pack_bf16x2(y[2], y[3]);
         if (a.Y != nullptr) {
           if (yvec) {
-            bstore64(u32x2{y0, y1}, yr, eo * 2, bo * 2);
+            bstore64<NTS>(u32x2{y0, y1}, yr, eo * 2, bo * 2);
           } else if (ok) {
             uint16_t* yp = a.Y + m * out_dim + j0;
             const uint16_t yb[4] = {(uint16_t)(y0 & 0xffff), (uint16_t)(y0 >> 16),
@@ -338,12 +342,12 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
             if (valid) loss += diff * diff;
             d[r] = valid ? (a.scale * diff) * act_out_grad(out_act, acc[n][r], y[r]) : 0.f;
           }
-          bstore64(u32x2{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])}, dr, lane * 8,
+          bstore64<NTS>(u32x2{pack_bf16x2(d[0], d[1]), pack_bf16x2(d[2], d[3])}, dr, lane * 8,
                    (uint32_t)((n * SO + s) * 512));
         }
         if constexpr (MODE == FWD_STASH) {
           const rsrc_t cr = make_rsrc(a.cOut + row0 * OP, a.cOut ? (int64_t)vblk * 64 * OP : 0);
-          bstore128(__builtin_bit_cast(u32x4, acc[n]), cr, lane * 16,
+          bstore128<NTS>(__builtin_bit_cast(u32x4, acc[n]), cr, lane * 16,
                     (uint32_t)((n * SO + s) * 1024));
         }
       }
