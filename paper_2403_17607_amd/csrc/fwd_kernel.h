@@ -154,16 +154,21 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
   // its two strips exist, so A_{L-1} is never held whole and the second
   // activation buffer is free during those two layers.  The next tile's X
   // is requested into it there, hidden behind that work.
-  // The launcher picks FU != 0 only for inference with every layer
+  // The launcher picks FU 1 or 2 only for inference with every layer
   // resident, L >= 2, SO == 1 and in_dim a multiple of 8.
-  constexpr bool FUSE = FU != 0;
-  static_assert(!FUSE || (!XPF && MODE == FWD_INFER), "fused last layers: W >= 64, inference");
+  // Other inference nets of these widths (FU 3, 4; L >= 2, in_dim a
+  // multiple of 8) keep the layers apart, and the next tile's X is
+  // requested into the activation buffer the output layer does not read,
+  // hidden behind that layer.
+  constexpr bool FUSE = FU == 1 || FU == 2;
+  constexpr bool OXP = FU == 3 || FU == 4;
+  static_assert(FU == 0 || (!XPF && MODE == FWD_INFER), "early X fetch: W >= 64, inference");
   u32x4 xq0[XPF ? NT : 1][KBW], xq1[XPF ? NT : 1][KBW];
   u32x4 actA[NT][KBW], actB[NT][KBW];
   if constexpr (XPF) {
     if ((int)blockIdx.x < a.ntiles) load_x(blockIdx.x, xq0);
     if ((int)blockIdx.x + G < a.ntiles) load_x(blockIdx.x + G, xq1);
-  } else if constexpr (FUSE) {
+  } else if constexpr (FUSE || OXP) {
     if ((int)blockIdx.x < a.ntiles) load_xv(blockIdx.x, actA);
   }
   drain_and_sync();  // weights (the first layer, when streaming) in LDS
@@ -202,7 +207,7 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) bx[n][kb] = xq[n][kb];
       if (tile + 2 * G < a.ntiles) load_x(tile + 2 * G, xq);
-    } else if constexpr (!F) {
+    } else if constexpr (!F && !OXP) {
       load_x(tile, bx);
     }
 
@@ -308,7 +313,14 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
         const uint32_t y0 = pack_bf16x2(y[0], y[1]), y1 = pack_bf16x2(y[2], y[3]);
         if (a.Y != nullptr) {
           if (yvec) {
-            bstore64<NTS>(u32x2{y0, y1}, yr, eo * 2, bo * 2);
+            // Y rows wider than one strip are completed by several stores,
+            // which the caches must merge: inference stores them with the
+            // default policy then (measured: width 64, out 64, 189 -> 80 us
+            // at 2^20 rows).
+            if (MODE == FWD_INFER && NTS && SO == 1)
+              bstore64<true>(u32x2{y0, y1}, yr, eo * 2, bo * 2);
+            else
+              bstore64<NTS && MODE != FWD_INFER>(u32x2{y0, y1}, yr, eo * 2, bo * 2);
           } else if (ok) {
             uint16_t* yp = a.Y + m * out_dim + j0;
             const uint16_t yb[4] = {(uint16_t)(y0 & 0xffff), (uint16_t)(y0 >> 16),
@@ -353,8 +365,8 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       }
     };
 
-    // Output layer on its own.
-    auto output = [&](const u32x4 (&in)[NT][KBW]) {
+    // Output layer on its own; with OXP the next tile's X goes to nx.
+    auto output = [&](const u32x4 (&in)[NT][KBW], u32x4 (&nx)[NT][KBW]) {
       const int l = L - 1;
       const u32x4* wl;
       if (resident) {
@@ -362,6 +374,9 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       } else {
         wl = stream_buf(step);
         stage_next(l, tile);
+      }
+      if constexpr (OXP) {
+        if (tile + G < a.ntiles) load_xv(tile + G, nx);
       }
       for (int s = 0; s < SO; ++s) {
         u32x4 af[KBW];
@@ -442,9 +457,9 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
       }
       if (l < L - 1) {
         hidden(I0{}, l, bx, by);
-        output(by);
+        output(by, bx);
       } else {
-        output(bx);
+        output(bx, by);
       }
     }
   };
@@ -468,6 +483,13 @@ __global__ __launch_bounds__(TileCfg<W>::NW * 64) void fwd_kernel(const FwdArgs 
   } else if constexpr (FU == 1) {
     using Fu = std::integral_constant<bool, true>;
     for (int tile = blockIdx.x; tile < a.ntiles; tile += G) tile_body(tile, actA, actB, Fu{}, xq0);
+  } else if constexpr (FU == 4) {
+    // L odd: the output layer reads the buffer the tile started in, so the
+    // next X lands in the other one and the loop alternates.
+    for (int tile = blockIdx.x; tile < a.ntiles; tile += 2 * G) {
+      tile_body(tile, actA, actB, NoF{}, xq0);
+      if (tile + G < a.ntiles) tile_body(tile + G, actB, actA, NoF{}, xq0);
+    }
   } else {
     for (int tile = blockIdx.x; tile < a.ntiles; tile += G) tile_body(tile, actA, actB, NoF{}, xq0);
   }
@@ -503,6 +525,9 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
   if constexpr (MODE == FWD_INFER && W >= 64) {
     if (a.resident && a.L >= 2 && SO == 1 && (a.in_dim % 8) == 0)
       kern = (a.L & 1) ? fwd_kernel<W, ACT, MODE, 1, true> : fwd_kernel<W, ACT, MODE, 2, true>;
+    else if (a.L >= 2 && (a.in_dim % 8) == 0)
+      kern = a.resident ? ((a.L & 1) ? fwd_kernel<W, ACT, MODE, 4, true> : fwd_kernel<W, ACT, MODE, 3, true>)
+                        : ((a.L & 1) ? fwd_kernel<W, ACT, MODE, 4, false> : fwd_kernel<W, ACT, MODE, 3, false>);
   }
   if constexpr (MODE == FWD_INFER && W <= 64) {
     // Small batches: fewer than two of the usual row tiles per CU (widths

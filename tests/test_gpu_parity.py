@@ -78,7 +78,7 @@ def test_activations(ffmlp, gpu, act, out_act):
 
 
 @pytest.mark.parametrize("width,depth", [(64, 0), (64, 1), (64, 2), (64, 16), (128, 16), (64, 24),
-                                         (16, 0), (128, 0), (32, 7)])
+                                         (128, 5), (16, 0), (128, 0), (32, 7)])
 def test_depths(ffmlp, gpu, width, depth):
     run_case(ffmlp, gpu, width, depth, width, width, 1000, seed=5)
 
