@@ -301,7 +301,7 @@ static hipError_t launch_t(const BwdArgs& a0, hipStream_t stream) {
   hipError_t e = device_info(&di);
   if (e != hipSuccess) return e;
   const size_t res_bytes = (size_t)a.total_frags * 1024;
-  a.resident = res_bytes + 1024 <= (size_t)di.max_lds ? 1 : 0;
+  a.resident = res_bytes <= (size_t)di.max_lds ? 1 : 0;  // the kernel has no static LDS
   size_t lds = a.resident ? res_bytes : (size_t)2 * a.layH_frags * 1024;
   if (lds == 0) lds = 16;
   auto kern = a.resident ? bwd_kernel<W, ACT, SEEDED, true, false> : bwd_kernel<W, ACT, SEEDED, false, false>;

@@ -83,6 +83,13 @@ def test_depths(ffmlp, gpu, width, depth):
     run_case(ffmlp, gpu, width, depth, width, width, 1000, seed=5)
 
 
+def test_weights_filling_all_of_lds(ffmlp, gpu):
+    """Width 128, 5 matrices of 128 x 128: the packed forward weights take
+    exactly 160 KiB, all of LDS; inference keeps them resident, the training
+    forward streams them."""
+    run_case(ffmlp, gpu, 128, 4, 128, 128, 3000, seed=24)
+
+
 @pytest.mark.parametrize("width,depth,in_dim,out_dim", [(16, 100, 16, 16), (32, 60, 5, 9)])
 def test_deep_nets(ffmlp, gpu, width, depth, in_dim, out_dim):
     """Deep sine nets (the weights stream through LDS layer by layer, and the
