@@ -24,6 +24,10 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   using C = WgCfg<W>;
   constexpr int TBK = C::TBK, TBJ = C::TBJ, GJ = C::GJ, KS = C::KS, KSW = C::KSW;
   constexpr int CH = wg_chunk<W>();
+  // Chunk loads are non-temporal at widths up to 32: every byte is read
+  // once (training step at 2^20 rows: width 16 188 -> 165 us, width 32
+  // 290 -> 265 us); at width 128 the same policy measured 2-5% slower.
+  constexpr int kLoadPol = W <= 32 ? 2 : 0;
   constexpr int LDT = CH + 8;      // LDS row stride (bf16) of the transposed tiles
   constexpr int LDW = LDT / 2;     // the same in 32-bit words
   constexpr int UPT = CH * W / 8 / 256;  // 16-byte units per thread per tensor
@@ -112,9 +116,9 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
     const __amdgpu_buffer_rsrc_t ra_src =
         xmode ? rsrc(a.X, c0, in_dim * 2, xvec ? M : 0) : rsrc(asrc, c0, W * 2, a.M16);
 #pragma unroll
-    for (int k = 0; k < UPT; ++k) ra[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(ra_src, voa[k], 0, 0));
+    for (int k = 0; k < UPT; ++k) ra[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(ra_src, voa[k], 0, kLoadPol));
 #pragma unroll
-    for (int k = 0; k < UPT; ++k) rd[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rd_src, vod[k], 0, 0));
+    for (int k = 0; k < UPT; ++k) rd[k] = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rd_src, vod[k], 0, kLoadPol));
   };
 
   // ---- registers -> LDS, transposed to [feature][batch row] ----
