@@ -83,6 +83,27 @@ def test_depths(ffmlp, gpu, width, depth):
     run_case(ffmlp, gpu, width, depth, width, width, 1000, seed=5)
 
 
+def _random_shapes(n, seed=2024):
+    """Seeded shapes across the launch variants: every width, depths 0-6,
+    in/out widths that are and are not multiples of 8 (vector or scalar X
+    and Y paths), every activation pair, ragged batches."""
+    import random
+    rng = random.Random(seed)
+    acts = ["linear", "relu", "sigmoid", "sine"]
+    out = []
+    for _ in range(n):
+        w = rng.choice([16, 32, 64, 128])
+        out.append((w, rng.randint(0, 6), rng.randint(1, w), rng.randint(1, w), rng.choice(acts),
+                    rng.choice(acts), rng.randint(1, 2600)))
+    return out
+
+
+@pytest.mark.parametrize("width,depth,in_dim,out_dim,act,out_act,M", _random_shapes(16))
+def test_random_shapes(ffmlp, gpu, width, depth, in_dim, out_dim, act, out_act, M):
+    run_case(ffmlp, gpu, width, depth, in_dim, out_dim, M, act=act, out_act=out_act,
+             seed=width + depth + in_dim + out_dim + M)
+
+
 def test_weights_filling_all_of_lds(ffmlp, gpu):
     """Width 128, 5 matrices of 128 x 128: the packed forward weights take
     exactly 160 KiB, all of LDS; inference keeps them resident, the training
