@@ -262,6 +262,12 @@ def test_input_gradient(ffmlp, gpu, width, depth, in_dim, out_dim, act, out_act)
     dx_case(ffmlp, gpu, width, depth, in_dim, out_dim, 4097, act, out_act)
 
 
+@pytest.mark.parametrize("width,depth,in_dim,out_dim,act,out_act,M", _random_shapes(8, seed=77))
+def test_random_shapes_input_gradient(ffmlp, gpu, width, depth, in_dim, out_dim, act, out_act, M):
+    dx_case(ffmlp, gpu, width, depth, in_dim, out_dim, M, act=act, out_act=out_act,
+            seed=width + depth + in_dim + out_dim + M)
+
+
 def test_input_gradient_streaming(ffmlp, gpu):
     """Weights too large for LDS (staged layer by layer) with dX."""
     dx_case(ffmlp, gpu, 128, 16, 128, 128, 3000)
