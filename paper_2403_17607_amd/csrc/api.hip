@@ -81,7 +81,7 @@ PackGeom pack_geom(const mlp* h) {
 // Workspace layout for a batch of M rows (byte offsets, 256-byte aligned).
 struct WsLayout {
   int64_t M16;
-  size_t stashA, stashS, reluMask, deltaH, deltaOut, cOut, partial, mid, lossPart, total;
+  size_t stashA, stashS, reluMask, deltaH, deltaOut, cOut, partial, lossPart, total;
   int P, chunks_per_block;
 };
 
@@ -111,7 +111,6 @@ WsLayout ws_layout(const mlp* h, int64_t M) {
   int64_t params = 0;
   for (int l = 0; l < L; ++l) params += (int64_t)fan_in_of(h, l) * fan_out_of(h, l);
   w.partial = o; o = round_up(o + (size_t)P * params * 4, 256);
-  w.mid = o; o = round_up(o + (size_t)kReduceSlices * params * 4, 256);
   w.lossPart = o; o = round_up(o + (size_t)kMaxLossParts * 4, 256);
   w.total = o;
   return w;
@@ -199,7 +198,6 @@ int run_wgrad_reduce(const mlp* h, const uint16_t* X, const WsLayout& w, uint8_t
   }
   ReduceArgs r{};
   r.partial = reinterpret_cast<const float*>(ws + w.partial);
-  r.mid = reinterpret_cast<float*>(ws + w.mid);
   r.G = G;
   r.params = params;
   r.P = M > 0 ? w.P : 0;

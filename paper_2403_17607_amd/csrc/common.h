@@ -142,13 +142,12 @@ struct WgradArgs {
   int P, chunks_per_block;
 };
 
-// Fixed-order sum of the P weight-gradient partials in two passes: pass 1
-// adds slice y (partials [y P / S, (y+1) P / S)) into mid[y]; pass 2 adds
-// the S slices in order into G and sums the loss partials.
+// Fixed-order sum of the P weight-gradient partials: slice y (partials
+// [y P / S, (y+1) P / S)) is added in order, then the S slice sums in order
+// into G; the same kernel sums the loss partials.
 constexpr int kReduceSlices = 16;
 struct ReduceArgs {
   const float* partial;  // [P][params]
-  float* mid;            // [kReduceSlices][params]
   float* G;
   int64_t params;
   int P;

@@ -256,52 +256,57 @@ __global__ __launch_bounds__(256) void wgrad_kernel(const WgradArgs a) {
   }
 }
 
-// Pass 1: mid[y][e] = sum of partial[p][e] over slice y of p, in order.
-__global__ __launch_bounds__(256) void reduce1_kernel(const ReduceArgs a) {
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int y = blockIdx.y;
-  if (e >= a.params) return;
-  const int p0 = (int)((int64_t)a.P * y / kReduceSlices);
-  const int p1 = (int)((int64_t)a.P * (y + 1) / kReduceSlices);
-  // Loads go out eight at a time, then are added in order: the same sum,
-  // without one memory latency per partial.
-  const float* src = a.partial + e;
-  float s = 0.f;
-  int p = p0;
-  for (; p + 8 <= p1; p += 8) {
-    float v[8];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) v[k] = src[(int64_t)(p + k) * a.params];
-#pragma unroll
-    for (int k = 0; k < 8; ++k) s += v[k];
-  }
-  for (; p < p1; ++p) s += src[(int64_t)p * a.params];
-  a.mid[(int64_t)y * a.params + e] = s;
-}
-
-// Pass 2: G[e] = sum over the slices in order.  The last block instead sums
-// the loss partials: thread t adds partials t, t + 256, ... in order, then a
-// fixed tree over the 256 threads.
-__global__ __launch_bounds__(256) void reduce2_kernel(const ReduceArgs a) {
+// Fixed-order sum of the P partials into G, one pass.  Block b owns
+// parameters 64 b .. 64 b + 63 and its wave y (of 16) adds slice y of the
+// partials, [y P / 16, (y + 1) P / 16), in order; the 16 slice sums are then
+// added in order through LDS.  The last block instead sums the loss
+// partials: thread t < 256 adds partials t, t + 256, ... in order, then a
+// fixed tree over those 256 threads.
+static_assert(kReduceSlices * 64 == 1024, "one wave per slice in a 1024-thread block");
+__global__ __launch_bounds__(1024) void reduce_kernel(const ReduceArgs a) {
+  __shared__ float part[kReduceSlices][64];
+  const int t = threadIdx.x;
   if (blockIdx.x == gridDim.x - 1) {
-    __shared__ float part[256];
-    float s = 0.f;
-    for (int i = threadIdx.x; i < a.nloss; i += 256) s += a.lossPart[i];
-    part[threadIdx.x] = s;
+    float* lp = &part[0][0];  // 256 of its 1024 floats
+    if (t < 256) {
+      float s = 0.f;
+      for (int i = t; i < a.nloss; i += 256) s += a.lossPart[i];
+      lp[t] = s;
+    }
     __syncthreads();
     for (int h = 128; h > 0; h >>= 1) {
-      if ((int)threadIdx.x < h) part[threadIdx.x] += part[threadIdx.x + h];
+      if (t < h) lp[t] += lp[t + h];
       __syncthreads();
     }
-    if (threadIdx.x == 0 && a.loss != nullptr) *a.loss = part[0] * a.loss_scale;
+    if (t == 0 && a.loss != nullptr) *a.loss = lp[0] * a.loss_scale;
     return;
   }
-  const int64_t e = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  const int j = t & 63, y = t >> 6;
+  const int64_t e = (int64_t)blockIdx.x * 64 + j;
+  float s = 0.f;
   if (e < a.params) {
-    float s = 0.f;
+    const int p0 = (int)((int64_t)a.P * y / kReduceSlices);
+    const int p1 = (int)((int64_t)a.P * (y + 1) / kReduceSlices);
+    // Loads go out eight at a time, then are added in order: the same sum,
+    // without one memory latency per partial.
+    const float* src = a.partial + e;
+    int p = p0;
+    for (; p + 8 <= p1; p += 8) {
+      float v[8];
 #pragma unroll
-    for (int y = 0; y < kReduceSlices; ++y) s += a.mid[(int64_t)y * a.params + e];
-    a.G[e] = s;
+      for (int k = 0; k < 8; ++k) v[k] = src[(int64_t)(p + k) * a.params];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) s += v[k];
+    }
+    for (; p < p1; ++p) s += src[(int64_t)p * a.params];
+  }
+  part[y][j] = s;
+  __syncthreads();
+  if (t < 64 && e < a.params) {
+    float g = 0.f;
+#pragma unroll
+    for (int k = 0; k < kReduceSlices; ++k) g += part[k][t];
+    a.G[e] = g;
   }
 }
 
@@ -391,12 +396,8 @@ hipError_t launch_wgrad(int width, const WgradArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s) {
-  int64_t blocks = (a.params + 255) / 256;
-  if (blocks < 1) blocks = 1;
-  hipLaunchKernelGGL(reduce1_kernel, dim3((unsigned)blocks, kReduceSlices), dim3(256), 0, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL(reduce2_kernel, dim3((unsigned)blocks + 1), dim3(256), 0, s, a);
+  const int64_t blocks = (a.params + 63) / 64;  // plus one for the loss
+  hipLaunchKernelGGL(reduce_kernel, dim3((unsigned)blocks + 1), dim3(1024), 0, s, a);
   return hipGetLastError();
 }
 
