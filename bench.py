@@ -140,9 +140,9 @@ def main():
                          "cache); hot: one X and T buffer every step")
     args = ap.parse_args()
     if args.gpus != 1:
-        print("bench.py runs on one GPU only: this build has no multi-GPU path "
-              "(inference shards rows with no communication; training would add one "
-              "all-reduce of the gradients).", file=sys.stderr)
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(inference would shard rows with no communication; training would add "
+              "one all-reduce of the gradients).", file=sys.stderr)
         sys.exit(2)
 
     import torch
