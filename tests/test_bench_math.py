@@ -1,0 +1,36 @@
+"""The benchmark's counting rules (no GPU): flops and algorithmic HBM bytes
+per row, pinned to values worked out by hand from the definitions.
+
+Flops count real dimensions only: the forward is 2 sum fan_in fan_out per
+row; the training step adds the backward without the first layer's input
+delta and the weight gradients (as many flops as the forward).  Bytes per
+row of the three-kernel training step: 4 in + 4 out + 8 d W + 6 OP (OP =
+out rounded up to 16), plus the derivative source of the hidden layers:
+ReLU masks 2 16 d, sigmoid activations re-read 2 d W, sine cos written and
+read 4 d W, linear nothing."""
+import bench
+
+
+def test_flops_per_row_sweep_shapes():
+    # (width, inference, training) for in = width, out 16, 4 hidden layers
+    for w, inf, train in [(16, 2560, 7168), (32, 9216, 25600), (64, 34816, 96256),
+                          (128, 135168, 372736)]:
+        assert bench.flops_per_row(w, 4, w, 16) == (inf, train)
+
+
+def test_flops_per_row_small_cases():
+    # depth 0: one in x out matrix, no backward product at all
+    assert bench.flops_per_row(64, 0, 40, 12) == (2 * 480, 4 * 480)
+    # depth 16, in/out 128: 17 matrices of 128 x 128
+    assert bench.flops_per_row(128, 16, 128, 128) == (557056, 557056 * 3 - 2 * 16384)
+
+
+def test_training_bytes_per_row():
+    base = lambda w, d, i, o: 4 * i + 4 * o + 8 * d * w + 6 * ((o + 15) // 16 * 16)
+    assert bench.train_bytes_per_row(128, 4, 128, 16, "relu") == 4896
+    assert bench.train_bytes_per_row(16, 4, 16, 16, "relu") == 864
+    assert bench.train_bytes_per_row(128, 4, 128, 16, "linear") == base(128, 4, 128, 16) == 4768
+    assert bench.train_bytes_per_row(128, 4, 128, 16, "sigmoid") == 4768 + 2 * 4 * 128
+    assert bench.train_bytes_per_row(128, 4, 128, 16, "sine") == 4768 + 4 * 4 * 128
+    # out 3 pads to one 16-column strip for the output delta
+    assert bench.train_bytes_per_row(64, 2, 64, 3, "relu") == base(64, 2, 64, 3) + 2 * 16 * 2
