@@ -50,16 +50,20 @@ __device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], const u32x
 // SMALL: one 16-row block per wave (inference on batches that give the
 // usual tiles fewer than two per compute unit, widths up to 64): four
 // times as many workgroups, so more waves share each CU's latency.
-// Waves per workgroup: inference at widths up to 32 streams X and Y with
-// little arithmetic per byte and runs 8 waves (more bytes in flight per CU:
-// width 16 at 2^22 rows 66 -> 56 us); every other case uses the tile
-// configuration.  The row tile changes with it; the stash layout does not.
-template <int W, int MODE>
-constexpr int fwd_waves() { return (W <= 32 && MODE == FWD_INFER) ? 8 : TileCfg<W>::NW; }
+// Waves per workgroup: inference at widths up to 32, and the small-batch
+// variant at any width, stream X and Y with little arithmetic per byte and
+// run 8 waves (more bytes in flight per CU: width 16 at 2^22 rows 66 -> 56
+// us, width 64 at 2^17 rows 12.6 -> 11.0 us); every other case uses the
+// tile configuration.  The row tile changes with it; the stash layout
+// does not.
+template <int W, int MODE, bool SMALL = false>
+constexpr int fwd_waves() {
+  return ((W <= 32 || SMALL) && MODE == FWD_INFER) ? 8 : TileCfg<W>::NW;
+}
 
 template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false>
-__global__ __launch_bounds__((fwd_waves<W, MODE>() * 64)) void fwd_kernel(const FwdArgs a) {
-  constexpr int NT = SMALL ? 1 : TileCfg<W>::NT, NW = fwd_waves<W, MODE>();
+__global__ __launch_bounds__((fwd_waves<W, MODE, SMALL>() * 64)) void fwd_kernel(const FwdArgs a) {
+  constexpr int NT = SMALL ? 1 : TileCfg<W>::NT, NW = fwd_waves<W, MODE, SMALL>();
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
   extern __shared__ u32x4 smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -520,7 +524,7 @@ __global__ __launch_bounds__((fwd_waves<W, MODE>() * 64)) void fwd_kernel(const 
 
 template <int W, int ACT, int MODE>
 static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out) {
-  constexpr int NTH = fwd_waves<W, MODE>() * 64;
+  int NTH = fwd_waves<W, MODE>() * 64;
   FwdArgs a = a0;
   if constexpr (fwd_waves<W, MODE>() != TileCfg<W>::NW) {
     const int64_t rows = (int64_t)TileCfg<W>::NT * fwd_waves<W, MODE>() * 16;
@@ -555,7 +559,8 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
     const int64_t cfg_rows = (int64_t)TileCfg<W>::NT * TileCfg<W>::NW * 16;
     if ((a.M + cfg_rows - 1) / cfg_rows <= 2 * (int64_t)di.cus && a.resident) {
       kern = fwd_kernel<W, ACT, MODE, 0, true, true>;
-      const int64_t rows = (int64_t)fwd_waves<W, MODE>() * 16;
+      NTH = fwd_waves<W, MODE, true>() * 64;
+      const int64_t rows = (int64_t)fwd_waves<W, MODE, true>() * 16;
       a.ntiles = (int)((a.M + rows - 1) / rows);
     }
   }
