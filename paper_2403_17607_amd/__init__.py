@@ -114,6 +114,29 @@ def _ptr(t) -> int | None:
     return t.data_ptr()
 
 
+def _require(t, name: str, dtype, shape=None, min_numel=None, device=None) -> None:
+    """Raise ValueError unless tensor `t` is a contiguous GPU tensor of
+    `dtype` (and `shape`, at least `min_numel` elements, on `device`).  The
+    C ABI derives every offset from M and the handle's dims and cannot see
+    buffer sizes, so these checks are what stands between a short or
+    mistyped buffer and an out-of-bounds access on the GPU; they run before
+    any launch and survive `python -O`."""
+    if not isinstance(t, torch.Tensor):
+        raise ValueError(f"{name} must be a torch.Tensor")
+    if not t.is_cuda:
+        raise ValueError(f"{name} must be on the GPU")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    if min_numel is not None and t.numel() < min_numel:
+        raise ValueError(f"{name} holds {t.numel()} elements, needs at least {min_numel}")
+    if device is not None and t.device != device:
+        raise ValueError(f"{name} is on {t.device}, the other arguments on {device}")
+
+
 def _stream(device) -> int:
     return torch.cuda.current_stream(device).cuda_stream
 
@@ -176,9 +199,10 @@ class FusedMLP:
     # -------------------------------------------------------------- calls --
     def pack(self, W: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
         """Pack bf16 weights [param_count] (concatenated row-major matrices)."""
-        assert W.dtype == torch.bfloat16 and W.numel() == self.param_count()
+        _require(W, "W", torch.bfloat16, shape=(self.param_count(),))
         if out is None:
             out = torch.empty(self.packed_bytes(), dtype=torch.uint8, device=W.device)
+        _require(out, "packed", torch.uint8, min_numel=self.packed_bytes(), device=W.device)
         _check(lib().mlp_pack_weights(self._h, _ptr(W), _ptr(out), _stream(W.device)))
         return out
 
@@ -186,10 +210,13 @@ class FusedMLP:
                 stash: torch.Tensor | None = None) -> torch.Tensor:
         """Algorithm 1.  X bf16 [M, in_dim] -> Y bf16 [M, out_dim].  With a
         training workspace as `stash`, also keeps the activations."""
-        assert X.dtype == torch.bfloat16 and X.dim() == 2 and X.shape[1] == self.in_dim
-        M = X.shape[0]
+        M = self._check_x(X)
+        self._check_packed(packed, X.device)
         if Y is None:
             Y = torch.empty(M, self.out_dim, dtype=torch.bfloat16, device=X.device)
+        _require(Y, "Y", torch.bfloat16, shape=(M, self.out_dim), device=X.device)
+        if stash is not None:
+            self._check_ws(stash, M, X.device, "stash")
         _check(lib().mlp_forward(self._h, _ptr(packed), _ptr(X), _ptr(Y), M, _ptr(stash),
                                  _stream(X.device)))
         return Y
@@ -198,9 +225,13 @@ class FusedMLP:
                  ws: torch.Tensor, G: torch.Tensor | None = None) -> torch.Tensor:
         """Weight gradients for a caller-given dY (fp32 [M, out_dim]) after
         forward(..., stash=ws)."""
-        assert dY.dtype == torch.float32 and dY.shape == (X.shape[0], self.out_dim)
+        M = self._check_x(X)
+        self._check_packed(packed, X.device)
+        _require(dY, "dY", torch.float32, shape=(M, self.out_dim), device=X.device)
+        self._check_ws(ws, M, X.device)
         if G is None:
             G = torch.empty(self.param_count(), dtype=torch.float32, device=X.device)
+        _require(G, "G", torch.float32, shape=(self.param_count(),), device=X.device)
         _check(lib().mlp_backward(self._h, _ptr(packed), _ptr(X), _ptr(dY), _ptr(G), X.shape[0],
                                   _ptr(ws), _stream(X.device)))
         return G
@@ -209,7 +240,7 @@ class FusedMLP:
                  packed: torch.Tensor | None, lr: float) -> None:
         """master -= lr G (fp32); W = bf16(master); re-packs into `packed`
         when given."""
-        self._check_params(master, G, W)
+        self._check_params(master, G, W, packed)
         _check(lib().mlp_sgd_step(self._h, _ptr(master), _ptr(G), _ptr(W), _ptr(packed), lr,
                                   _stream(master.device)))
 
@@ -218,31 +249,50 @@ class FusedMLP:
                   betas=(0.9, 0.999), eps: float = 1e-8, t: int = 1) -> None:
         """One Adam step t (1, 2, ...) on fp32 master weights and moments;
         W = bf16(master); re-packs into `packed` when given."""
-        self._check_params(master, G, W)
-        for b in (m, v):
-            assert b.dtype == torch.float32 and b.numel() == self.param_count() and b.is_contiguous()
+        self._check_params(master, G, W, packed)
+        for name, b in (("m", m), ("v", v)):
+            _require(b, name, torch.float32, shape=(self.param_count(),), device=master.device)
         _check(lib().mlp_adam_step(self._h, _ptr(master), _ptr(m), _ptr(v), _ptr(G), _ptr(W),
                                    _ptr(packed), lr, betas[0], betas[1], eps, t,
                                    _stream(master.device)))
 
-    def _check_params(self, master, G, W):
+    # ------------------------------------------------- argument checks --
+    def _check_params(self, master, G, W, packed):
         n = self.param_count()
-        assert master.dtype == torch.float32 and master.numel() == n and master.is_contiguous()
-        assert G.dtype == torch.float32 and G.numel() == n and G.is_contiguous()
-        assert W.dtype == torch.bfloat16 and W.numel() == n and W.is_contiguous()
+        _require(master, "master", torch.float32, shape=(n,))
+        _require(G, "G", torch.float32, shape=(n,), device=master.device)
+        _require(W, "W", torch.bfloat16, shape=(n,), device=master.device)
+        if packed is not None:
+            self._check_packed(packed, master.device)
+
+    def _check_x(self, X) -> int:
+        """X must be bf16 [M, in_dim] on the GPU; returns M."""
+        if not isinstance(X, torch.Tensor) or X.dim() != 2:
+            raise ValueError("X must be a 2-D tensor [M, in_dim]")
+        _require(X, "X", torch.bfloat16, shape=(X.shape[0], self.in_dim))
+        return X.shape[0]
+
+    def _check_packed(self, packed, device):
+        _require(packed, "packed", torch.uint8, min_numel=self.packed_bytes(), device=device)
+
+    def _check_ws(self, ws, M, device, name="ws"):
+        _require(ws, name, torch.uint8, min_numel=self.workspace_bytes(M), device=device)
 
     def backward_dx(self, packed: torch.Tensor, X: torch.Tensor, dY: torch.Tensor,
                     ws: torch.Tensor, G: torch.Tensor | None = None,
                     dX: torch.Tensor | None = None):
         """backward() plus the input gradient dX (fp32 [M, in_dim]); returns
         (G, dX)."""
-        assert dY.dtype == torch.float32 and dY.shape == (X.shape[0], self.out_dim)
-        M = X.shape[0]
+        M = self._check_x(X)
+        self._check_packed(packed, X.device)
+        _require(dY, "dY", torch.float32, shape=(M, self.out_dim), device=X.device)
+        self._check_ws(ws, M, X.device)
         if G is None:
             G = torch.empty(self.param_count(), dtype=torch.float32, device=X.device)
+        _require(G, "G", torch.float32, shape=(self.param_count(),), device=X.device)
         if dX is None:
             dX = torch.empty(M, self.in_dim, dtype=torch.float32, device=X.device)
-        assert dX.dtype == torch.float32 and dX.shape == (M, self.in_dim) and dX.is_contiguous()
+        _require(dX, "dX", torch.float32, shape=(M, self.in_dim), device=X.device)
         _check(lib().mlp_backward_dx(self._h, _ptr(packed), _ptr(X), _ptr(dY), _ptr(G), _ptr(dX),
                                      M, _ptr(ws), _stream(X.device)))
         return G, dX
@@ -252,12 +302,19 @@ class FusedMLP:
                    loss: torch.Tensor | None = None):
         """Algorithm 2 with the MSE loss.  Returns (G, loss) as device
         tensors; Y, if given, receives the bf16 outputs."""
-        assert T.dtype == torch.float32 and T.shape == (X.shape[0], self.out_dim)
+        M = self._check_x(X)
         dev = X.device
+        self._check_packed(packed, dev)
+        _require(T, "T", torch.float32, shape=(M, self.out_dim), device=dev)
+        self._check_ws(ws, M, dev)
         if G is None:
             G = torch.empty(self.param_count(), dtype=torch.float32, device=dev)
+        _require(G, "G", torch.float32, shape=(self.param_count(),), device=dev)
         if loss is None:
             loss = torch.empty(1, dtype=torch.float32, device=dev)
+        _require(loss, "loss", torch.float32, min_numel=1, device=dev)
+        if Y is not None:
+            _require(Y, "Y", torch.bfloat16, shape=(M, self.out_dim), device=dev)
         _check(lib().mlp_train_step(self._h, _ptr(packed), _ptr(X), _ptr(T), _ptr(Y), _ptr(G),
                                     _ptr(loss), X.shape[0], _ptr(ws), _stream(dev)))
         return G, loss

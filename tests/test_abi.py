@@ -138,3 +138,17 @@ def test_null_and_bad_arguments_fail_before_any_launch(ffmlp):
     assert L.mlp_adam_step(h, fake, fake, fake, fake, fake, ctypes.c_void_p(0x1008), 1e-3, 0.9,
                            0.999, 1e-8, 1, None) == inv  # misaligned packed
     L.mlp_destroy(None)  # ignored
+
+
+def test_binding_rejects_host_tensors_before_any_call(ffmlp):
+    """The binding checks every tensor before calling into the library: a
+    host tensor is refused with ValueError (no pointer reaches the C ABI)."""
+    import torch
+    net = ffmlp.FusedMLP(32, 2, 32, 16, "relu")
+    X = torch.zeros(10, 32, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="GPU"):
+        net.forward(torch.zeros(net.packed_bytes(), dtype=torch.uint8), X)
+    with pytest.raises(ValueError, match="GPU"):
+        net.pack(torch.zeros(net.param_count(), dtype=torch.bfloat16))
+    with pytest.raises(ValueError):
+        net.forward(None, X[0])  # not 2-D

@@ -490,3 +490,42 @@ def test_argument_errors_on_device(ffmlp, gpu):
     with pytest.raises(ffmlp.FFMLPError) as e:
         net.forward(packed, Xd)
     assert e.value.code == ffmlp.MLP_ERR_INVALID_ARG
+
+
+def test_binding_size_and_dtype_checks(ffmlp, gpu):
+    """Buffers too small for M, wrong dtypes or shapes, and mixed devices are
+    refused with ValueError before anything is enqueued (the C ABI derives
+    every offset from M and cannot see buffer sizes)."""
+    net = ffmlp.FusedMLP(64, 2, 64, 16, "relu")
+    M = 300
+    W, X, T = inputs(15, 64, 2, 64, 16, M)
+    packed = net.pack(W.to(gpu))
+    Xd, Td = X.to(gpu), T.to(gpu)
+    ws = net.workspace(M, gpu)
+    small_ws = net.workspace(M // 2, gpu)
+    bad = [
+        lambda: net.train_step(packed, Xd, Td, small_ws),                        # workspace for M/2
+        lambda: net.forward(packed, Xd, stash=small_ws),
+        lambda: net.train_step(packed[:-1024], Xd, Td, ws),                      # short packed
+        lambda: net.train_step(packed, Xd, Td[:-1], ws),                         # T rows
+        lambda: net.train_step(packed, Xd, Td.double(), ws),                     # T dtype
+        lambda: net.train_step(packed, Xd.float(), Td, ws),                      # X dtype
+        lambda: net.train_step(packed, Xd[:, :32].contiguous(), Td, ws),         # X columns
+        lambda: net.train_step(packed, Xd, Td, ws, Y=torch.empty(M - 1, 16, dtype=torch.bfloat16,
+                                                                 device=gpu)),   # Y rows
+        lambda: net.forward(packed, Xd, Y=torch.empty(M, 16, dtype=torch.float32, device=gpu)),
+        lambda: net.backward(packed, Xd, torch.zeros(M, 15, device=gpu), ws),    # dY columns
+        lambda: net.backward_dx(packed, Xd, torch.zeros(M, 16, device=gpu), ws,
+                                dX=torch.empty(M, 63, device=gpu)),              # dX columns
+        lambda: net.train_step(packed, Xd, Td, ws, G=torch.empty(7, device=gpu)),  # G size
+        lambda: net.pack(W.to(gpu)[:-1]),                                        # W size
+        lambda: net.train_step(packed, Xd, T, ws),                               # T on the host
+    ]
+    for i, f in enumerate(bad):
+        with pytest.raises(ValueError):
+            f()
+            pytest.fail(f"case {i} was accepted")
+    torch.cuda.synchronize()
+    G, loss = net.train_step(packed, Xd, Td, ws)  # the good call still works
+    torch.cuda.synchronize()
+    assert torch.isfinite(G).all()
