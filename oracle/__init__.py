@@ -15,10 +15,14 @@ tests/test_oracle.py, against facts that do not come from the oracle):
                 give relu(X) bitwise; zero input; power-of-two homogeneity;
                 row permutation; brute force on 2x2 nets with hand-derived
                 scalar formulas.
-  backward /    pinned: finite differences of the loss (rounding off),
-  train_step    the 2x2 brute-force formulas, depth 0 against a library
-                matmul, the closed-form deltas of the identity net, and
-                additivity of G over a split batch.
+  backward /    pinned: finite differences of the loss (rounding off;
+  train_step    every hidden and output activation, ReLU output included),
+                the 2x2 brute-force formulas, depth 0 against a library
+                matmul (all four output derivatives), the closed-form deltas
+                of the identity net, rounding-on closed forms of depth-1 sine
+                and sigmoid nets (bf16 cos C and A (1 - A) from the rounded
+                A as the derivative sources), and additivity of G over a
+                split batch.
 """
 from __future__ import annotations
 

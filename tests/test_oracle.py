@@ -82,18 +82,26 @@ def test_depth0_forward_is_one_gemm(out_act):
     np.testing.assert_allclose(Y32, ref, rtol=1e-13, atol=1e-14)
 
 
-@pytest.mark.parametrize("out_act", [LINEAR, SIGMOID])
+@pytest.mark.parametrize("out_act", [LINEAR, SIGMOID, RELU, SINE])
 def test_depth0_gradient_is_one_gemm(out_act):
     """Depth 0, no rounding: G_1 = X^T D with D = 2 (Y - T) / (M out)
-    times sigma_out' -- one library matmul."""
+    times sigma_out'(C), C = X W_1 -- one library matmul.  The derivatives
+    are written out here: y (1 - y) for sigmoid, [C > 0] for ReLU (0 at the
+    kink), cos C for sine."""
     net = Net(width=32, depth=0, in_dim=20, out_dim=12, out_act=out_act,
               round_bf16=False)
     W, X, T = rand_net_inputs(net, 257)
     r = net.train_step(W, X, T)
     Y = r["Y32"]
+    C = X @ W.reshape(20, 12)
     D = 2 * (Y - T) / (X.shape[0] * net.out_dim)
     if out_act == SIGMOID:
         D = D * Y * (1 - Y)
+    elif out_act == RELU:
+        assert 0 < np.mean(C > 0) < 1
+        D = D * (C > 0)
+    elif out_act == SINE:
+        D = D * np.cos(C)
     np.testing.assert_allclose(r["G"].reshape(20, 12), X.T @ D, rtol=1e-12, atol=1e-15)
     np.testing.assert_allclose(r["loss"], np.mean((Y - T) ** 2), rtol=1e-12)
 
@@ -205,7 +213,26 @@ FD_CASES = [
     (3, 3, 4, 1, SINE, SINE),
     (4, 2, 4, 3, RELU, LINEAR),
     (2, 1, 3, 2, LINEAR, SIGMOID),
+    (3, 2, 3, 2, RELU, RELU),
+    (4, 1, 2, 3, SIGMOID, RELU),
 ]
+
+
+def away_from_relu_kinks(net, W, X, margin=1e-3):
+    """True when every pre-activation that goes through a ReLU (hidden or
+    output) is at least `margin` away from 0, so central differences with a
+    step of 1e-6 never cross a kink."""
+    acts = {LINEAR: lambda c: c, RELU: lambda c: np.maximum(c, 0), SIGMOID: lambda c: 1 / (1 + np.exp(-c)),
+            SINE: np.sin}
+    A = X
+    mats = net.split(W)
+    for l, Wl in enumerate(mats):
+        C = A @ Wl
+        a = net.act if l < len(mats) - 1 else net.out_act
+        if a == RELU and np.min(np.abs(C)) < margin:
+            return False
+        A = acts[a](C)
+    return True
 
 
 @pytest.mark.parametrize("case", FD_CASES)
@@ -217,16 +244,10 @@ def test_gradient_matches_finite_differences(case):
     W = rng.uniform(-1, 1, net.param_count())
     X = rng.uniform(-1, 1, (M, in_dim))
     T = rng.uniform(-1, 1, (M, out_dim))
-    if act == RELU:
-        # stay away from the kink: every hidden pre-activation |c| > 1e-3
-        for _ in range(100):
-            Xb = X.copy()
-            ok = True
-            for l, Wl in enumerate(net.split(W)[:-1]):
-                C = Xb @ Wl
-                if np.min(np.abs(C)) < 1e-3:
-                    ok = False
-                Xb = np.maximum(C, 0)
+    if RELU in (act, out_act):
+        # stay away from the kinks: every ReLU pre-activation |c| > 1e-3
+        for _ in range(200):
+            ok = away_from_relu_kinks(net, W, X)
             if ok:
                 break
             W = rng.uniform(-1, 1, net.param_count())
@@ -269,13 +290,9 @@ def test_input_gradient_matches_finite_differences(case):
     M = 5
     W = rng.uniform(-1, 1, net.param_count())
     X = rng.uniform(-1, 1, (M, in_dim))
-    if act == RELU:
-        for _ in range(100):
-            Xb, ok = X.copy(), True
-            for Wl in net.split(W)[:-1]:
-                C = Xb @ Wl
-                ok = ok and np.min(np.abs(C)) >= 1e-3
-                Xb = np.maximum(C, 0)
+    if RELU in (act, out_act):
+        for _ in range(200):
+            ok = away_from_relu_kinks(net, W, X)
             if ok:
                 break
             X = rng.uniform(-1, 1, (M, in_dim))
@@ -361,6 +378,56 @@ def test_identity_net_deltas_closed_form():
     for l in range(1, net.L - 1):
         np.testing.assert_allclose(G[l], R.T @ (Dout * mask), rtol=1e-12, atol=1e-18)
     np.testing.assert_allclose(G[-1], R.T @ Dout, rtol=1e-12, atol=1e-18)
+
+
+def dyadic(rng, shape):
+    """Values k / 128, |k| <= 127: exact in bf16, and every sum of their
+    products is exact in fp64 whatever the order, so library matmuls give
+    the oracle's pre-activations bit for bit."""
+    return rng.integers(-127, 128, size=shape).astype(np.float64) / 128
+
+
+@pytest.mark.parametrize("act", [SINE, SIGMOID])
+@pytest.mark.parametrize("out_act", [LINEAR, SIGMOID])
+def test_depth1_rounding_on_closed_form(act, out_act):
+    """One hidden layer, rounding on, written out by hand:
+        C_1 = X W_1 (exact), A_2 = bf16(sigma(C_1)),
+        Y32 = sigma_out(A_2 W_2), D_3 = bf16(2 (Y32 - T) / (M out) sigma_out'),
+        D_2 = bf16((D_3 W_2^T) * s), with s = bf16(cos C_1) for sine and
+              s = A_2 (1 - A_2) from the rounded A_2 for sigmoid,
+        G_1 = X^T D_2,  G_2 = A_2^T D_3.
+    Pins which value each derivative is taken from once rounding is on (the
+    finite-difference checks run with rounding off)."""
+    rng = np.random.default_rng(99 + act + 5 * out_act)
+    w, i, o, M = 8, 6, 3, 11
+    net = Net(width=w, depth=1, in_dim=i, out_dim=o, act=act, out_act=out_act)
+    W1, W2 = dyadic(rng, (i, w)), dyadic(rng, (w, o))
+    X = dyadic(rng, (M, i))
+    T = rng.uniform(-1, 1, (M, o)).astype(np.float32).astype(np.float64)
+    rne = np.vectorize(oracle.rne_bf16)
+    C1 = X @ W1
+    if act == SINE:
+        A2 = rne(np.sin(C1))
+        s = rne(np.cos(C1))
+    else:
+        A2 = rne(1 / (1 + np.exp(-C1)))
+        s = A2 * (1 - A2)
+    C2 = A2 @ W2
+    Y32 = 1 / (1 + np.exp(-C2)) if out_act == SIGMOID else C2
+    g = 2 * (Y32 - T) / (M * o)
+    D3 = rne(g * (Y32 * (1 - Y32) if out_act == SIGMOID else 1.0))
+    D2 = rne((D3 @ W2.T) * s)
+    r = net.train_step(np.concatenate([W1.ravel(), W2.ravel()]), X, T, want_deltas=True)
+    np.testing.assert_array_equal(r["Y"], rne(Y32))
+    np.testing.assert_array_equal(r["D"][1], D3)
+    np.testing.assert_array_equal(r["D"][0], D2)
+    G1, G2 = net.split(r["G"])
+    np.testing.assert_allclose(G1, X.T @ D2, rtol=1e-12, atol=1e-18)
+    np.testing.assert_allclose(G2, A2.T @ D3, rtol=1e-12, atol=1e-18)
+    # the readings differ from the alternatives: with an unrounded cos or an
+    # unrounded sigmoid in the derivative some delta would change
+    alt = np.cos(C1) if act == SINE else (1 / (1 + np.exp(-C1))) * (1 - 1 / (1 + np.exp(-C1)))
+    assert np.any(rne((D3 @ W2.T) * alt) != D2)
 
 
 def test_gradient_additive_over_batch_split():
