@@ -61,7 +61,9 @@ def test_tiny_config(ffmlp, gpu):
     Yref = r["ref"]["Y"]
     match = np.mean(f64(r["Y"]) == Yref)
     log(f"  bitwise-equal outputs: {match:.4f}")
-    assert match > 0.9
+    # the rounding points match, so only fp32-versus-fp64 sums that straddle
+    # a bf16 rounding boundary can differ (measured: 0.9998)
+    assert match > 0.99
 
 
 @pytest.mark.parametrize("width", [16, 32, 64, 128])
@@ -480,6 +482,42 @@ def test_full_size_sampled(ffmlp, gpu, width, depth, in_dim, out_dim, M):
     log("  grad errs", ["%.2e" % e for e in errs])
     del ws
     torch.cuda.empty_cache()
+
+
+@pytest.mark.parametrize("width,depth,in_dim,out_dim,M", [
+    (128, 4, 128, 16, 1 << 20),       # the benchmark's training step
+    (128, 16, 128, 128, 1 << 20),     # depth/width stress net (streamed weights)
+    (64, 4, 64, 16, (1 << 20) + 37),  # ragged tail
+    (16, 4, 16, 16, 1 << 22),         # the largest sweep batch at width 16
+])
+def test_train_step_full_batch(ffmlp, gpu, width, depth, in_dim, out_dim, M):
+    """The timed training call at benchmark sizes, where every workgroup
+    loops over many row tiles: Y on every row, every layer's G over the
+    full batch and the loss against the oracle's training step, and the
+    inference outputs bitwise equal to the training forward's."""
+    log(f"train-step full batch w={width} d={depth} in={in_dim} out={out_dim} M={M}")
+    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, "relu")
+    onet = oracle_net(width, depth, in_dim, out_dim, "relu")
+    W = datagen.xavier_weights(16, width, depth, in_dim, out_dim)
+    Xd = datagen.inputs_uniform(16, M, in_dim, device=gpu)
+    Td = datagen.targets_uniform(16, M, out_dim, device=gpu)
+    packed = net.pack(W.to(gpu))
+    ws = net.workspace(M, gpu)
+    Y = torch.empty(M, out_dim, dtype=torch.bfloat16, device=gpu)
+    G, loss = net.train_step(packed, Xd, Td, ws, Y=Y)
+    Yi = net.forward(packed, Xd)
+    torch.cuda.synchronize()
+    assert torch.equal(Yi, Y), "inference outputs differ from the training forward's"
+    X, T = Xd.cpu(), Td.cpu()
+    del ws, Xd, Td, Yi
+    torch.cuda.empty_cache()
+    ref = onet.train_step(W, X, T)
+    log("  output errs (all rows)", check_outputs(f64(Y), ref["Y"], onet.L))
+    errs = check_grads(f64(G), ref["G"], onet)
+    log("  grad errs (full batch)", ["%.2e" % e for e in errs])
+    lerr = abs(loss.item() - ref["loss"]) / ref["loss"]
+    log(f"  loss {loss.item():.7f} oracle {ref['loss']:.7f} rel err {lerr:.2e}")
+    assert lerr <= LOSS_TOL
 
 
 def test_argument_errors_on_device(ffmlp, gpu):
