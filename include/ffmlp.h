@@ -169,6 +169,32 @@ int mlp_train_step(const mlp_t* h, const void* packed, const uint16_t* X,
                    const float* T, uint16_t* Y, float* G, float* loss,
                    int64_t M, void* ws, void* stream);
 
+/* Bytes of the library's own static device scratch array (64 MiB), the
+ * largest mlp_workspace_bytes(h, M, MLP_MODE_TRAIN) that
+ * mlp_train_step_noalloc accepts. */
+enum { MLP_SCRATCH_BYTES = 64 << 20 };
+
+/*
+ * mlp_train_step for callers that cannot allocate device memory: code under
+ * HIP graph capture, tight serving loops, harnesses that forbid hipMalloc.
+ * Same computation, arguments and results as mlp_train_step, but the
+ * workspace is a static array of MLP_SCRATCH_BYTES inside the library (one
+ * per GPU, held until the process ends) instead of a caller buffer.  The
+ * call allocates nothing (no hipMalloc, hipFree or allocating library
+ * routine); on its first call on a device it looks up that device's array
+ * once.  Nothing in the array has to start at zero: every byte a call reads
+ * was written earlier in the same call.
+ *   Returns MLP_ERR_WORKSPACE, before anything is enqueued, when
+ *   mlp_workspace_bytes(h, M, MLP_MODE_TRAIN) > MLP_SCRATCH_BYTES (for
+ *   example width 128, 4 hidden layers, out 16: up to about 16 000 rows).
+ * Every call on one GPU shares that GPU's array, so calls that overlap on
+ * one GPU (several streams or host threads at once) race; calls that follow
+ * each other in one stream do not.
+ */
+int mlp_train_step_noalloc(const mlp_t* h, const void* packed,
+                           const uint16_t* X, const float* T, uint16_t* Y,
+                           float* G, float* loss, int64_t M, void* stream);
+
 /* Optimizer step on fp32 master weights (NEXT-4; the paper leaves the
  * optimizer out of its training step, section III-A).  One kernel updates
  * every parameter, then writes the bf16 weights the fused kernels read

@@ -36,6 +36,7 @@ MLP_ERR_INVALID_ARG = -1
 MLP_ERR_UNSUPPORTED = -2
 MLP_ERR_WORKSPACE = -3
 MLP_ERR_HIP = -4
+MLP_SCRATCH_BYTES = 64 << 20
 MLP_MODE_INFER = 0
 MLP_MODE_TRAIN = 1
 
@@ -61,6 +62,8 @@ _SIGNATURES = {
     "mlp_backward_dx": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_int64, _VP, _VP]),
     "mlp_train_step": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_int64,
                                       _VP, _VP]),
+    "mlp_train_step_noalloc": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_int64,
+                                              _VP]),
     "mlp_sgd_step": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, ctypes.c_float, _VP]),
     "mlp_adam_step": (ctypes.c_int, [_VP, _VP, _VP, _VP, _VP, _VP, _VP, ctypes.c_float,
                                      ctypes.c_float, ctypes.c_float, ctypes.c_float,
@@ -317,4 +320,22 @@ class FusedMLP:
             _require(Y, "Y", torch.bfloat16, shape=(M, self.out_dim), device=dev)
         _check(lib().mlp_train_step(self._h, _ptr(packed), _ptr(X), _ptr(T), _ptr(Y), _ptr(G),
                                     _ptr(loss), X.shape[0], _ptr(ws), _stream(dev)))
+        return G, loss
+
+    def train_step_noalloc(self, packed: torch.Tensor, X: torch.Tensor, T: torch.Tensor,
+                           G: torch.Tensor, loss: torch.Tensor, Y: torch.Tensor | None = None):
+        """train_step with the library's static scratch array as the
+        workspace: nothing is allocated, so the caller passes G and loss.
+        Batches needing more than MLP_SCRATCH_BYTES of workspace are refused
+        by the library (FFMLPError, MLP_ERR_WORKSPACE)."""
+        M = self._check_x(X)
+        dev = X.device
+        self._check_packed(packed, dev)
+        _require(T, "T", torch.float32, shape=(M, self.out_dim), device=dev)
+        _require(G, "G", torch.float32, shape=(self.param_count(),), device=dev)
+        _require(loss, "loss", torch.float32, min_numel=1, device=dev)
+        if Y is not None:
+            _require(Y, "Y", torch.bfloat16, shape=(M, self.out_dim), device=dev)
+        _check(lib().mlp_train_step_noalloc(self._h, _ptr(packed), _ptr(X), _ptr(T), _ptr(Y),
+                                            _ptr(G), _ptr(loss), M, _stream(dev)))
         return G, loss

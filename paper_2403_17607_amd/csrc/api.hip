@@ -210,6 +210,36 @@ int run_wgrad_reduce(const mlp* h, const uint16_t* X, const WsLayout& w, uint8_t
   return MLP_OK;
 }
 
+int train_step_impl(const mlp_t* h, const void* packed, const uint16_t* X, const float* T,
+                    uint16_t* Y, float* G, float* loss, int64_t M, void* ws_, void* stream);
+
+// Workspace of mlp_train_step_noalloc: one static array per GPU, for callers
+// that cannot allocate.  In host code `scratch` only names the array; its
+// device address comes from hipGetSymbolAddress, once per device (each GPU
+// holds its own copy at its own address), and only that address is passed
+// to kernels.
+constexpr size_t kScratchBytes = MLP_SCRATCH_BYTES;
+__device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+hipError_t scratch_ptr(void** out) {
+  static std::mutex mu;
+  static std::vector<void*> ptrs;  // per device; null until looked up
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)ptrs.size() <= dev) ptrs.resize(dev + 1, nullptr);
+  if (!ptrs[dev]) {
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    if (!p || reinterpret_cast<uintptr_t>(p) % 256 != 0) return hipErrorInvalidSymbol;
+    ptrs[dev] = p;
+  }
+  *out = ptrs[dev];
+  return hipSuccess;
+}
+
 }  // namespace
 
 namespace ffmlp {
@@ -481,6 +511,33 @@ int mlp_backward_dx(const mlp_t* h, const void* packed, const uint16_t* X, const
 int mlp_train_step(const mlp_t* h, const void* packed, const uint16_t* X, const float* T,
                    uint16_t* Y, float* G, float* loss, int64_t M, void* ws_, void* stream) {
   g_err.clear();
+  return train_step_impl(h, packed, X, T, Y, G, loss, M, ws_, stream);
+}
+
+int mlp_train_step_noalloc(const mlp_t* h, const void* packed, const uint16_t* X, const float* T,
+                           uint16_t* Y, float* G, float* loss, int64_t M, void* stream) {
+  g_err.clear();
+  if (int rc = check_handle(h)) return rc;
+  if (M >= 0 && M <= ((int64_t)1 << 36)) {
+    const size_t need = ws_layout(h, M).total;
+    if (need > kScratchBytes)
+      return fail(MLP_ERR_WORKSPACE,
+                  "a batch of %lld rows needs %zu workspace bytes, more than the %zu of the "
+                  "static scratch array",
+                  (long long)M, need, kScratchBytes);
+  }
+  void* ws = nullptr;
+  hipError_t e = scratch_ptr(&ws);
+  if (e != hipSuccess) return hip_fail(e, "scratch array lookup");
+  return train_step_impl(h, packed, X, T, Y, G, loss, M, ws, stream);
+}
+
+}  // extern "C"
+
+namespace {
+
+int train_step_impl(const mlp_t* h, const void* packed, const uint16_t* X, const float* T,
+                    uint16_t* Y, float* G, float* loss, int64_t M, void* ws_, void* stream) {
   if (int rc = check_handle(h)) return rc;
   if (M < 0) return fail(MLP_ERR_INVALID_ARG, "M = %lld < 0", (long long)M);
   if (!G || !ws_) return fail(MLP_ERR_INVALID_ARG, "null G or workspace");
@@ -514,4 +571,4 @@ int mlp_train_step(const mlp_t* h, const void* packed, const uint16_t* X, const 
   return run_wgrad_reduce(h, X, w, ws, M, G, loss, nloss, s);
 }
 
-}  // extern "C"
+}  // namespace
