@@ -108,9 +108,14 @@ WsLayout ws_layout(const mlp* h, int64_t M) {
   P = cpb > 0 ? (nch + cpb - 1) / cpb : 1;  // no empty workgroups
   w.P = (int)P;
   w.chunks_per_block = (int)cpb;
+  // The fused backward writes one partial per workgroup, at most one per
+  // row tile and at most kBwdgMaxBlocks.
+  int64_t Pf = (M + kBwdgRows - 1) / kBwdgRows;
+  if (Pf > kBwdgMaxBlocks) Pf = kBwdgMaxBlocks;
+  const int64_t Pmax = P > Pf ? P : Pf;
   int64_t params = 0;
   for (int l = 0; l < L; ++l) params += (int64_t)fan_in_of(h, l) * fan_out_of(h, l);
-  w.partial = o; o = round_up(o + (size_t)P * params * 4, 256);
+  w.partial = o; o = round_up(o + (size_t)Pmax * params * 4, 256);
   w.lossPart = o; o = round_up(o + (size_t)kMaxLossParts * 4, 256);
   w.total = o;
   return w;
@@ -175,6 +180,55 @@ BwdArgs bwd_args(const mlp* h, const void* packed, const WsLayout& w, uint8_t* w
   return b;
 }
 
+// Fixed-order sum of P weight-gradient partials (and the loss partials).
+int run_reduce(const mlp* h, const WsLayout& w, uint8_t* ws, int64_t M, int P, float* G,
+               float* loss, int nloss, hipStream_t s) {
+  ReduceArgs r{};
+  r.partial = reinterpret_cast<const float*>(ws + w.partial);
+  r.G = G;
+  r.params = param_count(h);
+  r.P = M > 0 ? P : 0;
+  r.lossPart = reinterpret_cast<const float*>(ws + w.lossPart);
+  r.nloss = M > 0 ? nloss : 0;
+  r.loss = loss;
+  r.loss_scale = M > 0 ? (float)(1.0 / ((double)M * h->out_dim)) : 0.f;
+  hipError_t e = launch_reduce(r, s);
+  if (e != hipSuccess) return hip_fail(e, "reduce kernel launch");
+  return MLP_OK;
+}
+
+// The fused backward pass with the weight gradients, then the reduce.
+// Returns 1 (nothing enqueued) when the fused kernel does not cover the net.
+int run_fused_backward(const mlp* h, const void* packed, const uint16_t* X, const float* dY,
+                       const WsLayout& w, uint8_t* ws, int64_t M, float* G, float* loss, int nloss,
+                       int seeded, hipStream_t s) {
+  if (M <= 0 || !backward_fused_supported(h->width, n_mats(h), h->act, h->in_dim, h->out_dim))
+    return 1;
+  const PackGeom g = pack_geom(h);
+  BwdgArgs a{};
+  a.packed = reinterpret_cast<const u32x4*>(static_cast<const uint8_t*>(packed) + (size_t)g.fwd_total * 1024);
+  a.X = X;
+  a.stashA = reinterpret_cast<const uint16_t*>(ws + w.stashA);
+  a.reluMask = reinterpret_cast<const uint32_t*>(ws + w.reluMask);
+  a.deltaOut = reinterpret_cast<const uint16_t*>(ws + w.deltaOut);
+  a.cOut = h->out_act != MLP_ACT_LINEAR ? reinterpret_cast<const float*>(ws + w.cOut) : nullptr;
+  a.dY = dY;
+  a.partial = reinterpret_cast<float*>(ws + w.partial);
+  a.M = M;
+  a.M16 = w.M16;
+  a.params = param_count(h);
+  a.in_dim = h->in_dim;
+  a.out_dim = h->out_dim;
+  a.out_act = h->out_act;
+  a.ntiles = (int)((M + kBwdgRows - 1) / kBwdgRows);
+  a.layH_frags = g.bwd_hidden;
+  int P = 0;
+  hipError_t e = launch_backward_fused(h->width, n_mats(h), h->out_dim, seeded, a, s, &P);
+  if (e == hipErrorNotSupported) return 1;
+  if (e != hipSuccess) return hip_fail(e, "fused backward kernel launch");
+  return run_reduce(h, w, ws, M, P, G, loss, nloss, s);
+}
+
 int run_wgrad_reduce(const mlp* h, const uint16_t* X, const WsLayout& w, uint8_t* ws, int64_t M,
                      float* G, float* loss, int nloss, hipStream_t s) {
   const int64_t params = param_count(h);
@@ -196,18 +250,7 @@ int run_wgrad_reduce(const mlp* h, const uint16_t* X, const WsLayout& w, uint8_t
     hipError_t e = launch_wgrad(h->width, a, s);
     if (e != hipSuccess) return hip_fail(e, "weight-gradient kernel launch");
   }
-  ReduceArgs r{};
-  r.partial = reinterpret_cast<const float*>(ws + w.partial);
-  r.G = G;
-  r.params = params;
-  r.P = M > 0 ? w.P : 0;
-  r.lossPart = reinterpret_cast<const float*>(ws + w.lossPart);
-  r.nloss = M > 0 ? nloss : 0;
-  r.loss = loss;
-  r.loss_scale = M > 0 ? (float)(1.0 / ((double)M * h->out_dim)) : 0.f;
-  hipError_t e = launch_reduce(r, s);
-  if (e != hipSuccess) return hip_fail(e, "reduce kernel launch");
-  return MLP_OK;
+  return run_reduce(h, w, ws, M, w.P, G, loss, nloss, s);
 }
 
 int train_step_impl(const mlp_t* h, const void* packed, const uint16_t* X, const float* T,
@@ -498,6 +541,10 @@ int mlp_backward_dx(const mlp_t* h, const void* packed, const uint16_t* X, const
   hipStream_t s = static_cast<hipStream_t>(stream);
   const WsLayout w = ws_layout(h, M);
   uint8_t* ws = static_cast<uint8_t*>(ws_);
+  if (!dX && n_mats(h) > 1) {
+    const int rc = run_fused_backward(h, packed, X, dY, w, ws, M, G, nullptr, 0, 1, s);
+    if (rc <= 0) return rc;
+  }
   if (M > 0) {
     BwdArgs b = bwd_args(h, packed, w, ws, M);
     b.dY = dY;
@@ -563,6 +610,8 @@ int train_step_impl(const mlp_t* h, const void* packed, const uint16_t* X, const
     hipError_t e = launch_forward(h->width, h->act, FWD_TRAIN, a, s, &nloss);
     if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
     if (n_mats(h) > 1) {
+      const int rc = run_fused_backward(h, packed, X, nullptr, w, ws, M, G, loss, nloss, 0, s);
+      if (rc <= 0) return rc;
       BwdArgs b = bwd_args(h, packed, w, ws, M);
       e = launch_backward(h->width, h->act, 0, b, s);
       if (e != hipSuccess) return hip_fail(e, "backward kernel launch");

@@ -1,0 +1,382 @@
+// Fused backward pass with the weight gradients: the delta loop of
+// Algorithm 2, D_i = sigma_b(A_i, D_{i+1} B_i^T), and the products
+// G_i = A_i^T D_{i+1} in one kernel (arXiv 2403.17607, section III-A; the
+// paper computes G outside its fused kernel and names fusing it into the
+// backward pass as future work in section V).  ReLU hidden layers.
+//
+// A workgroup of eight waves owns a tile of 128 batch rows at a time
+// (persistent loop over tiles).  Each wave carries the deltas of its own 16
+// rows through the layers in VGPRs exactly as the unfused backward kernel
+// does: chain order, backward-packed weights resident in LDS as the MFMA A
+// operand, ReLU masks from the forward pass.
+//
+// G_i is a contraction over the batch, so its MFMA operands need each lane
+// to hold batch rows of one feature, the transpose of the delta layout.
+// Both operands are brought to that form on the matrix cores: an MFMA whose
+// B operand is a 0/1 selection matrix returns a 16x16 block of its A operand
+// transposed, exactly (one bf16 product per output, all other terms zero).
+//   - Each wave writes its 16 rows of D_{i+1}, transposed, into an LDS tile
+//     DT[feature][row] of the 128 rows.
+//   - Each wave owns a fixed slice of every G_i (one 16-feature strip of A_i
+//     against one or more strips of D_{i+1}).  It reads its A_i strip for
+//     the tile's 128 rows straight from the activation stash, transposes it
+//     the same way and accumulates the slice over the tile from DT.
+// The slices stay in registers across all of the workgroup's tiles; at the
+// end the workgroup writes them as one fp32 partial G, which the fixed-order
+// reduce kernel adds to the other workgroups' partials.  The deltas never go
+// to HBM: per row the kernel reads the output delta, the ReLU masks, X and
+// the stashed activations once, and writes nothing.
+#pragma once
+
+#include "device.h"
+
+namespace ffmlp {
+
+template <int W, int L, int OS>
+struct BwdgGeom {
+  static constexpr int NW = kBwdgWaves, SW = W / 16, KBW = (W + 31) / 32;
+  static constexpr int KBO = (OS * 16 + 31) / 32;  // k-blocks of the output delta
+  static constexpr int LDT = kBwdgRows + 8;        // DT row stride (bf16): 68 words
+  // Resident fragments: backward layers 1 .. L-2 whole, then the output
+  // layer's first KBO k-blocks of each strip (past out_dim they are zero).
+  static constexpr int WFRAGS = (L - 2) * SW * KBW + SW * KBO;
+  static constexpr size_t lds_bytes() { return (size_t)WFRAGS * 1024 + (size_t)W * LDT * 2; }
+  static constexpr int woff(int l) { return (l - 1) * SW * KBW; }  // fragment offset, layer l >= 1
+  // Slices of G_l: SW k-strips (features of A_l) x sd(l) j-strips (of
+  // D_{l+1}) of 16x16 tiles; wave w owns tiles w tpw .. w tpw + tpw - 1
+  // (row-major over (k-strip, j-strip)), or tile w when there are fewer
+  // tiles than waves.
+  static constexpr int sd(int l) { return l == L - 1 ? OS : SW; }
+  static constexpr int ntl(int l) { return SW * sd(l); }
+  static constexpr int tpw(int l) { return ntl(l) >= NW ? ntl(l) / NW : 1; }
+  static constexpr int goff(int l) {
+    int o = 0;
+    for (int i = 0; i < l; ++i) o += tpw(i);
+    return o;
+  }
+  static constexpr int nacc() { return goff(L); }
+  static_assert(L >= 2 && L <= kBwdgMaxL, "fused backward: 2 .. kBwdgMaxL matrices");
+};
+
+template <int W, int L, int OS, int SEEDED>
+__global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a) {
+  using Gm = BwdgGeom<W, L, OS>;
+  constexpr int NW = Gm::NW, SW = Gm::SW, KBW = Gm::KBW, KBO = Gm::KBO, LDT = Gm::LDT;
+  constexpr int NACC = Gm::nacc();
+  constexpr int KS = kBwdgRows / 32;  // 32-row contraction steps per tile
+  extern __shared__ u32x4 smem[];
+  uint16_t* DT = reinterpret_cast<uint16_t*>(smem + (size_t)Gm::WFRAGS * 64);
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
+  const int li = lane & 15, lg = lane >> 4;
+  const int64_t M = a.M;
+  const int in_dim = a.in_dim, out_dim = a.out_dim, out_act = a.out_act;
+  const int SO = (out_dim + 15) >> 4;  // strips of the output (at most OS)
+  const int OP = SO * 16;
+  const bool yvec = (out_dim & 3) == 0;
+
+  // Resident weights (direct-to-LDS loads, waited for below).
+  stage_frags(smem, a.packed, (uint32_t)((L - 2) * SW * KBW), wave, NW, lane);
+  {
+    const u32x4* src = a.packed + (size_t)(L - 2) * a.layH_frags * 64;
+    u32x4* dst = smem + (size_t)Gm::woff(L - 1) * 64;
+    for (int f = wave; f < SW * KBO; f += NW) {
+      const int s = f / KBO, kb = f - s * KBO;
+      __builtin_amdgcn_global_load_lds(
+          (const void __attribute__((address_space(1)))*)(src + (size_t)(s * KBW + kb) * 64 + lane),
+          (void __attribute__((address_space(3)))*)(dst + (size_t)f * 64), 16, 0, 0);
+    }
+  }
+  // Selection matrices (MFMA B operands, lane (g, n) holds rows 8 g .. 8 g + 7
+  // of column n): sel0 picks contraction slot n - 4 g of group g, i.e. the
+  // four features a lane group holds in slots 0-3; sel1 the same in slots
+  // 4-7.  An A operand whose lane (g, i) holds batch row i with features
+  // 4 g + q in slots q (sel0) or 4 + q (sel1) then yields out[i][n] = that
+  // row's feature n, and the result lane (g, n) holds feature n of rows
+  // 4 g .. 4 g + 3: the 16x16 block transposed.
+  u32x4 sel0 = {0u, 0u, 0u, 0u}, sel1 = {0u, 0u, 0u, 0u};
+  {
+    const int q = li - 4 * lg;
+    if (q >= 0 && q < 4) {
+      const uint32_t one = 0x3F80u << (16 * (q & 1));  // bf16 1.0 in the slot's half
+      if (q < 2) {
+        sel0.x = one;
+        sel1.z = one;
+      } else {
+        sel0.y = one;
+        sel1.w = one;
+      }
+    }
+  }
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+
+  f32x4 gacc[NACC];
+#pragma unroll
+  for (int i = 0; i < NACC; ++i) gacc[i] = zero4;
+
+  // The wave's slice of G_l: its k-strip and first j-strip; false when the
+  // layer has fewer tiles than waves and this wave has none.
+  auto slice = [&](auto lc, int& kt, int& jt0) -> bool {
+    constexpr int l = decltype(lc)::value;
+    constexpr int sd = Gm::sd(l), ntl = Gm::ntl(l), tpw = Gm::tpw(l);
+    if constexpr (ntl >= NW) {
+      const int t0 = wave * tpw;
+      kt = t0 / sd;
+      jt0 = t0 % sd;
+      return true;
+    } else {
+      kt = wave / sd;
+      jt0 = wave % sd;
+      return wave < ntl;
+    }
+  };
+
+  drain_and_sync();  // weights in LDS
+
+  const int G = gridDim.x;
+  for (int tile = blockIdx.x; tile < a.ntiles; tile += G) {
+    const int64_t tr0 = (int64_t)tile * kBwdgRows;  // the tile's first row
+    const int64_t row0 = tr0 + wave * 16;            // this wave's 16 rows
+    const int64_t blk = row0 / 16;
+    int64_t vrows = M - row0;
+    vrows = vrows < 0 ? 0 : (vrows > 16 ? 16 : vrows);
+    const int vblk = vrows > 0 ? 1 : 0;
+    int64_t tb = (a.M16 - tr0) / 16;  // 16-row blocks of the tile inside the stash
+    const int tvblk = (int)(tb < 0 ? 0 : (tb > NW ? NW : tb));
+
+    // A_l strip of the wave's G_l slice, rows tr0 .. tr0 + 127, lane (g, i)
+    // of block b holding row 16 b + i, features 16 kt + 4 g .. + 3.
+    u32x2 ar[NW];
+    auto load_a = [&](auto lc) {
+      constexpr int l = decltype(lc)::value;
+      int kt, jt0;
+      if (!slice(lc, kt, jt0)) return;
+      if constexpr (l == 0) {
+        int64_t rows = M - tr0;
+        rows = rows < 0 ? 0 : (rows > kBwdgRows ? kBwdgRows : rows);
+        const rsrc_t xr = make_rsrc(a.X + tr0 * in_dim, rows * in_dim * 2);
+        const int f0 = 16 * kt + 4 * lg;
+        const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
+#pragma unroll
+        for (int b = 0; b < NW; ++b) ar[b] = bload64(xr, voff, (uint32_t)(b * 32 * in_dim));
+      } else {
+        const rsrc_t sr = make_rsrc(a.stashA + (size_t)(l - 1) * a.M16 * W + (size_t)tr0 * W,
+                                    (int64_t)tvblk * 32 * W);
+#pragma unroll
+        for (int b = 0; b < NW; ++b) ar[b] = bload64(sr, lane * 8, (uint32_t)((b * SW + kt) * 512));
+      }
+    };
+    auto load_mask = [&](int idx) -> uint32_t {
+      const rsrc_t mr = make_rsrc(a.reluMask + ((size_t)idx * (size_t)(a.M16 / 16) + blk) * 64,
+                                  vblk ? 256 : 0);
+      return bload32(mr, lane * 4, 0u);
+    };
+
+    // Output delta of the wave's rows, chain order.
+    u32x4 dA[KBW], dB[KBW];
+#pragma unroll
+    for (int kb = 0; kb < KBW; ++kb) dA[kb] = u32x4{0u, 0u, 0u, 0u};
+    {
+      const rsrc_t dr = make_rsrc(a.deltaOut + row0 * OP, SEEDED ? 0 : (int64_t)vblk * 32 * OP);
+      const rsrc_t cr = make_rsrc(a.cOut + row0 * OP, (SEEDED && a.cOut) ? (int64_t)vblk * 64 * OP : 0);
+      const rsrc_t gr = make_rsrc(a.dY + row0 * out_dim, (SEEDED && a.dY) ? vrows * out_dim * 4 : 0);
+      static_for<0, OS>([&](auto sc) {
+        constexpr int s = decltype(sc)::value;
+        if (s >= SO) return;
+        uint32_t p0, p1;
+        if constexpr (!SEEDED) {
+          const u32x2 v = bload64(dr, lane * 8, (uint32_t)(s * 512));
+          p0 = v.x;
+          p1 = v.y;
+        } else {
+          const int64_t m = row0 + li;
+          const int j0 = s * 16 + lg * 4;
+          float g[4] = {0.f, 0.f, 0.f, 0.f};
+          if (yvec) {
+            const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
+            const u32x4 v = bload128(gr, eo * 4, 0u);
+            g[0] = __uint_as_float(v.x);
+            g[1] = __uint_as_float(v.y);
+            g[2] = __uint_as_float(v.z);
+            g[3] = __uint_as_float(v.w);
+          } else if (m < M && j0 < out_dim) {
+            const float* dp = a.dY + m * out_dim + j0;
+#pragma unroll
+            for (int r = 0; r < 4; ++r)
+              if (j0 + r < out_dim) g[r] = dp[r];
+          }
+          if (out_act != ACT_LINEAR) {
+            const u32x4 cv = bload128(cr, lane * 16, (uint32_t)(s * 1024));
+            const float c[4] = {__uint_as_float(cv.x), __uint_as_float(cv.y),
+                                __uint_as_float(cv.z), __uint_as_float(cv.w)};
+#pragma unroll
+            for (int r = 0; r < 4; ++r) g[r] *= act_out_grad(out_act, c[r], act_apply(out_act, c[r]));
+          }
+          p0 = pack_bf16x2(g[0], g[1]);
+          p1 = pack_bf16x2(g[2], g[3]);
+        }
+        if constexpr (s & 1) {
+          dA[s >> 1].z = p0;
+          dA[s >> 1].w = p1;
+        } else {
+          dA[s >> 1].x = p0;
+          dA[s >> 1].y = p1;
+        }
+      });
+    }
+    uint32_t mw = load_mask(L - 2);  // relu'(a_{L-1})
+    load_a(std::integral_constant<int, L - 1>{});
+
+    // Layer l: D_{l+1} (in `cur`) into DT; D_l = (D_{l+1} W_l^T) relu'(a_l)
+    // into `nxt`; the wave's slice of G_l = A_l^T D_{l+1} over the tile.
+    auto layer_step = [&](auto lc, u32x4 (&cur)[KBW], u32x4 (&nxt)[KBW]) {
+      constexpr int l = decltype(lc)::value;
+      constexpr int SD = Gm::sd(l);
+      static_for<0, SD>([&](auto sc) {
+        constexpr int s = decltype(sc)::value;
+        const f32x4 o = mfma16(cur[s >> 1], (s & 1) ? sel1 : sel0, zero4);
+        const u32x2 v = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+        // rows 4 g .. 4 g + 3 of block `wave`: positions 8 g + 4 (wave % 2)
+        // of contraction step wave / 2, so that a contraction operand is one
+        // 16-byte read holding the rows in the transposed A operand's order
+        *reinterpret_cast<u32x2*>(DT + (16 * s + li) * LDT + 32 * (wave >> 1) + 8 * lg + 4 * (wave & 1)) = v;
+      });
+      if constexpr (l >= 1) {
+        constexpr int KBL = (l == L - 1) ? KBO : KBW;  // contraction over D_{l+1}'s features
+        const u32x4* wl = smem + (size_t)Gm::woff(l) * 64;
+        if constexpr (SW == 1) {
+          nxt[0].z = 0u;
+          nxt[0].w = 0u;
+        }
+        static_for<0, SW>([&](auto sc) {
+          constexpr int s = decltype(sc)::value;
+          u32x4 af[KBL];
+#pragma unroll
+          for (int kb = 0; kb < KBL; ++kb) af[kb] = wl[(s * KBL + kb) * 64 + lane];
+          f32x4 acc = zero4;
+#pragma unroll
+          for (int kb = 0; kb < KBL; ++kb) acc = mfma16(af[kb], cur[kb], acc);
+          // relu'(a) is [a > 0]: zero the rounded products where a is 0
+          const uint32_t t = mw >> (2 * s);
+          const uint32_t p0 = mask_halves(pack_bf16x2(acc[0], acc[1]), t & 0x00010001u);
+          const uint32_t p1 = mask_halves(pack_bf16x2(acc[2], acc[3]), (t >> 1) & 0x00010001u);
+          if constexpr (s & 1) {
+            nxt[s >> 1].z = p0;
+            nxt[s >> 1].w = p1;
+          } else {
+            nxt[s >> 1].x = p0;
+            nxt[s >> 1].y = p1;
+          }
+          __builtin_amdgcn_sched_barrier(0);
+        });
+        if constexpr (l >= 2) mw = load_mask(l - 2);
+      }
+      __syncthreads();  // DT holds D_{l+1} of all 128 rows
+      int kt, jt0;
+      if (slice(lc, kt, jt0)) {
+        // A_l strip transposed: step ks holds rows 4 g + r of blocks 2 ks
+        // (slots r) and 2 ks + 1 (slots 4 + r), feature 16 kt + n in lane
+        // (g, n), the order the DT writes above used
+        u32x4 aop[KS];
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const u32x4 src = {ar[2 * ks].x, ar[2 * ks].y, ar[2 * ks + 1].x, ar[2 * ks + 1].y};
+          const f32x4 o0 = mfma16(src, sel0, zero4);
+          const f32x4 o1 = mfma16(src, sel1, zero4);
+          aop[ks] = u32x4{pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3]),
+                          pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
+        }
+        if constexpr (l >= 1) load_a(std::integral_constant<int, l - 1>{});
+        constexpr int TPW = Gm::tpw(l), GO = Gm::goff(l);
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+#pragma unroll
+          for (int u = 0; u < TPW; ++u) {
+            const u32x4 bop =
+                *reinterpret_cast<const u32x4*>(DT + (16 * (jt0 + u) + li) * LDT + 32 * ks + 8 * lg);
+            gacc[GO + u] = mfma16(aop[ks], bop, gacc[GO + u]);
+          }
+        }
+      } else {
+        if constexpr (l >= 1) load_a(std::integral_constant<int, l - 1>{});
+      }
+      __syncthreads();  // every wave is done reading DT
+    };
+
+    static_for<0, L>([&](auto ic) {
+      constexpr int l = L - 1 - decltype(ic)::value;
+      if constexpr (((L - 1 - l) & 1) == 0)
+        layer_step(std::integral_constant<int, l>{}, dA, dB);
+      else
+        layer_step(std::integral_constant<int, l>{}, dB, dA);
+    });
+  }
+
+  // The workgroup's partial G, in the weights' layout (each element of G is
+  // in exactly one wave's slice).
+  float* part = a.partial + (size_t)blockIdx.x * (size_t)a.params;
+  static_for<0, L>([&](auto lc) {
+    constexpr int l = decltype(lc)::value;
+    constexpr int TPW = Gm::tpw(l), GO = Gm::goff(l);
+    int kt, jt0;
+    if (!slice(lc, kt, jt0)) return;
+    const int fi = l == 0 ? in_dim : W, fo = l == L - 1 ? out_dim : W;
+    const int64_t off = l == 0 ? 0 : (int64_t)in_dim * W + (int64_t)(l - 1) * W * W;
+#pragma unroll
+    for (int u = 0; u < TPW; ++u) {
+      const int j = 16 * (jt0 + u) + li;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int k = 16 * kt + 4 * lg + r;
+        if (k < fi && j < fo) part[off + (int64_t)k * fo + j] = gacc[GO + u][r];
+      }
+    }
+  });
+}
+
+template <int W, int L, int OS, int SEEDED>
+static hipError_t bwdg_launch_t(const BwdgArgs& a, hipStream_t stream, int* grid_out) {
+  using Gm = BwdgGeom<W, L, OS>;
+  DeviceInfo di;
+  hipError_t e = device_info(&di);
+  if (e != hipSuccess) return e;
+  const size_t lds = Gm::lds_bytes();
+  if (lds > (size_t)di.max_lds) return hipErrorNotSupported;
+  auto kern = bwdg_kernel<W, L, OS, SEEDED>;
+  int occ = 0;
+  e = kernel_occupancy(reinterpret_cast<const void*>(kern), kBwdgWaves * 64, lds, &occ);
+  if (e != hipSuccess) return e;
+  int grid = di.cus * occ;
+  if (grid > a.ntiles) grid = a.ntiles;
+  if (grid > kBwdgMaxBlocks) grid = kBwdgMaxBlocks;
+  if (grid < 1) grid = 1;
+  *grid_out = grid;
+  hipLaunchKernelGGL(kern, dim3(grid), dim3(kBwdgWaves * 64), lds, stream, a);
+  return hipGetLastError();
+}
+
+template <int W, int OS>
+static hipError_t bwdg_by_l(int L, int seeded, const BwdgArgs& a, hipStream_t s, int* g) {
+  switch (L) {
+    case 2: return seeded ? bwdg_launch_t<W, 2, OS, 1>(a, s, g) : bwdg_launch_t<W, 2, OS, 0>(a, s, g);
+    case 3: return seeded ? bwdg_launch_t<W, 3, OS, 1>(a, s, g) : bwdg_launch_t<W, 3, OS, 0>(a, s, g);
+    case 4: return seeded ? bwdg_launch_t<W, 4, OS, 1>(a, s, g) : bwdg_launch_t<W, 4, OS, 0>(a, s, g);
+    case 5: return seeded ? bwdg_launch_t<W, 5, OS, 1>(a, s, g) : bwdg_launch_t<W, 5, OS, 0>(a, s, g);
+    default: return hipErrorNotSupported;
+  }
+}
+
+// Output-strip classes compiled per width: the kernel's register slices of
+// the output layer's G are sized for OS strips.
+template <int W>
+constexpr int bwdg_os(int out_dim) {
+  if constexpr (W == 128) return out_dim <= 16 ? 1 : 0;  // 0: not compiled
+  else if constexpr (W == 64) return out_dim <= 16 ? 1 : 4;
+  else return W / 16;
+}
+
+template <int W>
+hipError_t launch_backward_fused_w(int L, int out_dim, int seeded, const BwdgArgs& a, hipStream_t s,
+                                   int* grid_out);
+
+}  // namespace ffmlp

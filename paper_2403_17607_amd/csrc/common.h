@@ -131,6 +131,28 @@ struct BwdArgs {
   uint32_t layH_frags, total_frags;
 };
 
+// Fused backward pass with the weight gradients (bwdg_kernel): the deltas
+// never go to HBM; each workgroup keeps fixed slices of every layer's G in
+// registers across its row tiles and writes them once, as one partial.
+constexpr int kBwdgWaves = 8;        // waves per workgroup, 16 rows each
+constexpr int kBwdgRows = 16 * kBwdgWaves;  // rows per tile
+constexpr int kBwdgMaxBlocks = 512;  // at most this many partials
+constexpr int kBwdgMaxL = 5;         // weight matrices of the largest fused net
+struct BwdgArgs {
+  const u32x4* packed;       // backward-packed weights, layers 1 .. L-1
+  const uint16_t* X;         // [M][in_dim]
+  const uint16_t* stashA;    // (L-1) x [M16][W] tile images: a_1 .. a_{L-1}
+  const uint32_t* reluMask;  // (L-1) x [M16/16][64] ReLU mask words
+  const uint16_t* deltaOut;  // [M16][OP] output delta (training step)
+  const float* cOut;         // [M16][OP] fp32 pre-activation (seeded, nonlinear output)
+  const float* dY;           // [M][out_dim] (seeded mode)
+  float* partial;            // [gridDim.x][params]
+  int64_t M, M16, params;
+  int in_dim, out_dim, out_act;
+  int ntiles;                // kBwdgRows-row tiles
+  uint32_t layH_frags;       // 1 KiB fragments of one packed hidden layer
+};
+
 struct WgradArgs {
   const uint16_t* X;
   const uint16_t* stashA;
@@ -183,6 +205,13 @@ hipError_t launch_forward(int width, int act, int mode, const FwdArgs& a,
 hipError_t launch_backward(int width, int act, int seeded, const BwdArgs& a,
                            hipStream_t s);
 hipError_t launch_wgrad(int width, const WgradArgs& a, hipStream_t s);
+// Fused backward pass and weight-gradient partials; *grid_out receives the
+// number of partials written.  hipErrorNotSupported when no instantiation
+// covers the net (the caller then runs the unfused kernels).
+hipError_t launch_backward_fused(int width, int L, int out_dim, int seeded, const BwdgArgs& a,
+                                 hipStream_t s, int* grid_out);
+// Whether launch_backward_fused covers a net (host-side shape check only).
+bool backward_fused_supported(int width, int L, int act, int in_dim, int out_dim);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_optim(const OptArgs& a, hipStream_t s);

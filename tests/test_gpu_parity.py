@@ -247,10 +247,13 @@ def dx_case(ffmlp, dev, width, depth, in_dim, out_dim, M, act="relu", out_act="l
     G, dX = net.backward_dx(packed, Xd, dYd, ws)
     G0 = net.backward(packed, Xd, dYd, ws)
     torch.cuda.synchronize()
-    assert torch.equal(G, G0), "G differs between mlp_backward_dx and mlp_backward"
     Gref, dXref = onet.backward_dx(W, X, dY)
     log("  dx errs", check_dx(f64(dX), dXref, onet.L))
     check_grads(f64(G), Gref, onet)
+    # mlp_backward may take the fused kernel (another summation order of G)
+    check_grads(f64(G0), Gref, onet)
+    d = (G - G0).norm() / G0.norm().clamp_min(1e-30)
+    assert d.item() < 1e-5, "G of mlp_backward_dx and mlp_backward differ beyond fp32 rounding"
 
 
 @pytest.mark.parametrize("width,depth,in_dim,out_dim,act,out_act", [
