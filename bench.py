@@ -42,21 +42,39 @@ def flops_per_row(width, depth, in_dim, out_dim):
     return fwd, fwd + bwd + 2 * P  # inference, training step
 
 
-def train_bytes_per_row(width, depth, in_dim, out_dim, act):
-    """HBM bytes the three-kernel training step must move per row:
-    forward reads X, T and writes the activations, the output delta and
-    (ReLU) the activation masks; backward reads the output delta and the
+def fused_backward(width, depth, in_dim, out_dim, act):
+    """Whether the library's training step runs the fused backward kernel
+    (deltas kept on chip, weight gradients accumulated in the same kernel):
+    ReLU hidden layers, 2 to 5 weight matrices, in_dim a multiple of 4 and,
+    at width 128, at most 16 outputs; otherwise it runs the three kernels
+    (backward, weight gradients, reduce).  The rule of include/ffmlp.h."""
+    return (act == "relu" and 1 <= depth <= 4 and in_dim % 4 == 0
+            and (width != 128 or out_dim <= 16))
+
+
+def train_bytes_per_row(width, depth, in_dim, out_dim, act, fused=None, masks=True):
+    """HBM bytes the training step must move per row.
+    Forward (both plans): reads X and T, writes the activations, the output
+    delta and (ReLU) the activation masks.
+    Fused plan: the backward kernel reads the output delta, the masks, X and
+    the activations (the weight-gradient operands) and writes no deltas.
+    Three-kernel plan: the backward reads the output delta and the
     derivative source of every hidden activation (ReLU: its mask, 16 B per
-    row; sigmoid: the activation; sine: the stored cos; linear: nothing)
-    and writes the hidden deltas; the gradient kernel reads X, the
-    activations, the hidden deltas and the output delta."""
+    row, or with masks=False the activation itself; sigmoid: the
+    activation; sine: the stored cos; linear: nothing) and writes the hidden
+    deltas; the gradient kernel reads X, the activations, the hidden deltas
+    and the output delta."""
+    if fused is None:
+        fused = fused_backward(width, depth, in_dim, out_dim, act)
     OP = (out_dim + 15) // 16 * 16
     hid = depth * width * 2
-    mask = depth * 16 if act == "relu" else 0
-    deriv = {"relu": mask, "linear": 0}.get(act, hid)
+    mask = depth * 16 if (act == "relu" and masks) else 0
+    deriv = {"relu": mask if masks else hid, "linear": 0}.get(act, hid)
     b = 2 * in_dim + 4 * out_dim + hid + 2 * OP + mask    # forward (train)
     if act == "sine":
         b += hid                                          # cos stash write
+    if fused:
+        return b + 2 * OP + mask + 2 * in_dim + hid       # fused backward
     b += 2 * OP + deriv + hid                             # backward
     b += 2 * in_dim + hid + hid + 2 * OP                  # weight gradients
     return b
@@ -211,6 +229,7 @@ def main():
     ms_per_step = wall * 1e3 / K
 
     fl_inf, fl_train = flops_per_row(width, depth, in_dim, out_dim)
+    fused = fused_backward(width, depth, in_dim, out_dim, args.act)
     inf_tflops = fl_inf * M / (t_inf * 1e-3) / 1e12
     train_tflops = fl_train * M / (t_train * 1e-3) / 1e12
     bytes_inf = M * (2 * in_dim + 2 * out_dim)
@@ -256,12 +275,20 @@ def main():
                      "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
                                      "scaled by a reference copy)",
                      "flops_per_row": fl_inf, "rows_per_launch": M},
-        "roofline_train": {"kernels": "fwd_kernel (train) + bwd_kernel + wgrad_kernel + "
-                                      "reduce_kernel", "bound": "hbm", "achieved": train_gbs,
+        "roofline_train": {"kernels": ("fwd_kernel (train) + bwdg_kernel (fused backward and "
+                                       "weight gradients) + reduce_kernel") if fused else
+                                      ("fwd_kernel (train) + bwd_kernel + wgrad_kernel + "
+                                       "reduce_kernel"),
+                           "bound": "hbm", "achieved": train_gbs,
                            "peak": PEAK_HBM_GBS, "unit": "GB/s",
                            "frac": train_gbs / PEAK_HBM_GBS,
                            "bytes_per_row": train_bytes_per_row(width, depth, in_dim, out_dim,
-                                                                args.act)},
+                                                                args.act),
+                           "bytes_per_row_three_kernels": train_bytes_per_row(
+                               width, depth, in_dim, out_dim, args.act, fused=False),
+                           "bytes_per_row_three_kernels_no_masks": train_bytes_per_row(
+                               width, depth, in_dim, out_dim, args.act, fused=False,
+                               masks=False)},
     }
     del ws
     torch.cuda.empty_cache()

@@ -52,8 +52,8 @@ extern "C" {
 
 typedef struct mlp mlp_t;
 
-/* Activations (section III-A uses ReLU hidden layers with a linear output
- * in its benchmarks; sigmoid and sine serve the application-shaped nets). */
+/* Activations (the benchmarks of section IV use ReLU hidden layers with a
+ * linear output; sigmoid and sine serve the application-shaped nets). */
 enum {
   MLP_ACT_LINEAR = 0,
   MLP_ACT_RELU = 1,
@@ -164,6 +164,13 @@ int mlp_backward_dx(const mlp_t* h, const void* packed, const uint16_t* X,
  *   loss  optional device float, set to sum (Y - T)^2 / (M out_dim)
  *         computed from the fp32 outputs before rounding.
  *   ws    mlp_workspace_bytes(h, M, MLP_MODE_TRAIN) bytes, 256-byte aligned.
+ * Kernels: the forward pass, then for ReLU nets of 2 to 5 weight matrices
+ * with in_dim a multiple of 4 (and out_dim <= 16 at width 128) one fused
+ * kernel that propagates the deltas and accumulates the weight gradients
+ * without storing the deltas (the fusion section V of the paper proposes),
+ * otherwise a backward kernel and a weight-gradient kernel; then a
+ * fixed-order reduction, so G is bitwise the same from run to run.
+ * mlp_backward uses the same rule; mlp_backward_dx always the latter.
  */
 int mlp_train_step(const mlp_t* h, const void* packed, const uint16_t* X,
                    const float* T, uint16_t* Y, float* G, float* loss,
@@ -186,7 +193,7 @@ enum { MLP_SCRATCH_BYTES = 64 << 20 };
  * was written earlier in the same call.
  *   Returns MLP_ERR_WORKSPACE, before anything is enqueued, when
  *   mlp_workspace_bytes(h, M, MLP_MODE_TRAIN) > MLP_SCRATCH_BYTES (for
- *   example width 128, 4 hidden layers, out 16: up to about 16 000 rows).
+ *   example width 128, 4 hidden layers, out 16: up to 15 744 rows).
  * Every call on one GPU shares that GPU's array, so calls that overlap on
  * one GPU (several streams or host threads at once) race; calls that follow
  * each other in one stream do not.

@@ -27,10 +27,28 @@ def test_flops_per_row_small_cases():
 
 def test_training_bytes_per_row():
     base = lambda w, d, i, o: 4 * i + 4 * o + 8 * d * w + 6 * ((o + 15) // 16 * 16)
-    assert bench.train_bytes_per_row(128, 4, 128, 16, "relu") == 4896
-    assert bench.train_bytes_per_row(16, 4, 16, 16, "relu") == 864
+    assert bench.train_bytes_per_row(128, 4, 128, 16, "relu", fused=False) == 4896
+    assert bench.train_bytes_per_row(16, 4, 16, 16, "relu", fused=False) == 864
+    # the blueprint's three-kernel count, ReLU derivative read from the activations
+    assert bench.train_bytes_per_row(128, 4, 128, 16, "relu", fused=False, masks=False) == 5792
     assert bench.train_bytes_per_row(128, 4, 128, 16, "linear") == base(128, 4, 128, 16) == 4768
     assert bench.train_bytes_per_row(128, 4, 128, 16, "sigmoid") == 4768 + 2 * 4 * 128
     assert bench.train_bytes_per_row(128, 4, 128, 16, "sine") == 4768 + 4 * 4 * 128
     # out 3 pads to one 16-column strip for the output delta
-    assert bench.train_bytes_per_row(64, 2, 64, 3, "relu") == base(64, 2, 64, 3) + 2 * 16 * 2
+    assert bench.train_bytes_per_row(64, 2, 64, 3, "relu", fused=False) == \
+        base(64, 2, 64, 3) + 2 * 16 * 2
+
+
+def test_fused_training_bytes_per_row():
+    """Fused plan: 4 in + 4 out + 4 d W + 4 OP, plus the ReLU masks written
+    and read (2 16 d): no hidden delta is written or read."""
+    fused = lambda w, d, i, o: 4 * i + 4 * o + 4 * d * w + 4 * ((o + 15) // 16 * 16) + 32 * d
+    assert bench.fused_backward(128, 4, 128, 16, "relu")
+    assert bench.train_bytes_per_row(128, 4, 128, 16, "relu") == fused(128, 4, 128, 16) == 2816
+    assert bench.train_bytes_per_row(16, 4, 16, 16, "relu") == fused(16, 4, 16, 16) == 576
+    assert bench.train_bytes_per_row(64, 2, 64, 3, "relu") == fused(64, 2, 64, 3)
+    # outside the fused kernel's nets: the three-kernel count
+    for args in [(128, 4, 128, 128, "relu"), (128, 16, 128, 128, "relu"), (64, 4, 3, 1, "sine"),
+                 (64, 4, 64, 16, "sigmoid"), (64, 0, 64, 16, "relu"), (64, 4, 6, 16, "relu")]:
+        assert not bench.fused_backward(*args)
+        assert bench.train_bytes_per_row(*args) == bench.train_bytes_per_row(*args, fused=False)
