@@ -16,7 +16,8 @@
 // B operand is a 0/1 selection matrix returns a 16x16 block of its A operand
 // transposed, exactly (one bf16 product per output, all other terms zero).
 //   - Each wave writes its 16 rows of D_{i+1}, transposed, into an LDS tile
-//     DT[feature][row] of the 128 rows.
+//     DT[feature][row] of the 128 rows (16-byte chunks XOR-swizzled by the
+//     feature row, so that its reads and writes are free of bank conflicts).
 //   - Each wave owns a fixed slice of every G_i (one 16-feature strip of A_i
 //     against one or more strips of D_{i+1}).  It reads its A_i strip for
 //     the tile's 128 rows straight from the activation stash, transposes it
@@ -36,7 +37,7 @@ template <int W, int L, int OS>
 struct BwdgGeom {
   static constexpr int NW = kBwdgWaves, SW = W / 16, KBW = (W + 31) / 32;
   static constexpr int KBO = (OS * 16 + 31) / 32;  // k-blocks of the output delta
-  static constexpr int LDT = kBwdgRows + 8;        // DT row stride (bf16): 68 words
+  static constexpr int LDT = kBwdgRows;            // DT row: 128 rows of bf16, 16 chunks of 16 B
   // Resident fragments: backward layers 1 .. L-2 whole, then the output
   // layer's first KBO k-blocks of each strip (past out_dim they are zero).
   static constexpr int WFRAGS = (L - 2) * SW * KBW + SW * KBO;
@@ -131,65 +132,100 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
     }
   };
 
+  // DT element offset of chunk c (8 bf16, one 16-byte contraction operand)
+  // of feature row f.  A row is 256 bytes, all 64 banks; chunk c is stored
+  // at chunk c ^ (f % 16), so the 16 lanes of a 16-byte read (16 feature
+  // rows, one chunk) and the 32 lanes of an 8-byte write (16 rows, two
+  // chunks, different halves where they meet) touch distinct banks.
+  auto dt_off = [&](int f, int c) { return f * LDT + ((c ^ (f & 15)) << 3); };
+
   drain_and_sync();  // weights in LDS
 
-  const int G = gridDim.x;
-  for (int tile = blockIdx.x; tile < a.ntiles; tile += G) {
-    const int64_t tr0 = (int64_t)tile * kBwdgRows;  // the tile's first row
-    const int64_t row0 = tr0 + wave * 16;            // this wave's 16 rows
-    const int64_t blk = row0 / 16;
-    int64_t vrows = M - row0;
-    vrows = vrows < 0 ? 0 : (vrows > 16 ? 16 : vrows);
-    const int vblk = vrows > 0 ? 1 : 0;
-    int64_t tb = (a.M16 - tr0) / 16;  // 16-row blocks of the tile inside the stash
-    const int tvblk = (int)(tb < 0 ? 0 : (tb > NW ? NW : tb));
+  // Rows of a tile: tr0 is its first row; this wave owns 16-row block `blk`
+  // (valid when vblk); tvblk of the tile's blocks lie inside the stash.
+  struct TileGeom {
+    int64_t tr0, row0, blk, vrows;
+    int vblk, tvblk;
+  };
+  auto geom = [&](int tile) {
+    TileGeom t;
+    t.tr0 = (int64_t)tile * kBwdgRows;
+    t.row0 = t.tr0 + wave * 16;
+    t.blk = t.row0 / 16;
+    int64_t v = M - t.row0;
+    t.vrows = v < 0 ? 0 : (v > 16 ? 16 : v);
+    t.vblk = t.vrows > 0 ? 1 : 0;
+    const int64_t tb = (a.M16 - t.tr0) / 16;
+    t.tvblk = (int)(tb < 0 ? 0 : (tb > NW ? NW : tb));
+    return t;
+  };
 
-    // A_l strip of the wave's G_l slice, rows tr0 .. tr0 + 127, lane (g, i)
-    // of block b holding row 16 b + i, features 16 kt + 4 g .. + 3.
-    u32x2 ar[NW];
-    auto load_a = [&](auto lc) {
-      constexpr int l = decltype(lc)::value;
-      int kt, jt0;
-      if (!slice(lc, kt, jt0)) return;
-      if constexpr (l == 0) {
-        int64_t rows = M - tr0;
-        rows = rows < 0 ? 0 : (rows > kBwdgRows ? kBwdgRows : rows);
-        const rsrc_t xr = make_rsrc(a.X + tr0 * in_dim, rows * in_dim * 2);
-        const int f0 = 16 * kt + 4 * lg;
-        const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
+  // A_l strip of the wave's G_l slice, rows tr0 .. tr0 + 127, lane (g, i)
+  // of block b holding row 16 b + i, features 16 kt + 4 g .. + 3.
+  u32x2 ar[NW];
+  auto load_a = [&](auto lc, const TileGeom& t) {
+    constexpr int l = decltype(lc)::value;
+    int kt, jt0;
+    if (!slice(lc, kt, jt0)) return;
+    if constexpr (l == 0) {
+      int64_t rows = M - t.tr0;
+      rows = rows < 0 ? 0 : (rows > kBwdgRows ? kBwdgRows : rows);
+      const rsrc_t xr = make_rsrc(a.X + t.tr0 * in_dim, rows * in_dim * 2);
+      const int f0 = 16 * kt + 4 * lg;
+      const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
 #pragma unroll
-        for (int b = 0; b < NW; ++b) ar[b] = bload64(xr, voff, (uint32_t)(b * 32 * in_dim));
-      } else {
-        const rsrc_t sr = make_rsrc(a.stashA + (size_t)(l - 1) * a.M16 * W + (size_t)tr0 * W,
-                                    (int64_t)tvblk * 32 * W);
+      for (int b = 0; b < NW; ++b) ar[b] = bload64(xr, voff, (uint32_t)(b * 32 * in_dim));
+    } else {
+      const rsrc_t sr = make_rsrc(a.stashA + (size_t)(l - 1) * a.M16 * W + (size_t)t.tr0 * W,
+                                  (int64_t)t.tvblk * 32 * W);
 #pragma unroll
-        for (int b = 0; b < NW; ++b) ar[b] = bload64(sr, lane * 8, (uint32_t)((b * SW + kt) * 512));
-      }
-    };
-    auto load_mask = [&](int idx) -> uint32_t {
-      const rsrc_t mr = make_rsrc(a.reluMask + ((size_t)idx * (size_t)(a.M16 / 16) + blk) * 64,
-                                  vblk ? 256 : 0);
-      return bload32(mr, lane * 4, 0u);
-    };
+      for (int b = 0; b < NW; ++b) ar[b] = bload64(sr, lane * 8, (uint32_t)((b * SW + kt) * 512));
+    }
+  };
+  auto load_mask = [&](int idx, const TileGeom& t) -> uint32_t {
+    const rsrc_t mr = make_rsrc(a.reluMask + ((size_t)idx * (size_t)(a.M16 / 16) + t.blk) * 64,
+                                t.vblk ? 256 : 0);
+    return bload32(mr, lane * 4, 0u);
+  };
+  // What a tile needs first, requested one tile ahead (during the previous
+  // tile's last layer): the output delta (training mode), the mask words of
+  // a_{L-1} and the A strip of layer L-1.
+  u32x2 dq[OS];
+  uint32_t mq = 0u;
+  auto fetch = [&](int tile) {
+    const TileGeom t = geom(tile);
+    if constexpr (!SEEDED) {
+      const rsrc_t dr = make_rsrc(a.deltaOut + t.row0 * OP, (int64_t)t.vblk * 32 * OP);
+#pragma unroll
+      for (int s = 0; s < OS; ++s)
+        dq[s] = bload64(dr, lane * 8, s < SO ? (uint32_t)(s * 512) : kOOB);
+    }
+    mq = load_mask(L - 2, t);
+    load_a(std::integral_constant<int, L - 1>{}, t);
+  };
+
+  const int G = gridDim.x;
+  if ((int)blockIdx.x < a.ntiles) fetch(blockIdx.x);
+  for (int tile = blockIdx.x; tile < a.ntiles; tile += G) {
+    const TileGeom t = geom(tile);
+    const bool more = tile + G < a.ntiles;
 
     // Output delta of the wave's rows, chain order.
     u32x4 dA[KBW], dB[KBW];
 #pragma unroll
     for (int kb = 0; kb < KBW; ++kb) dA[kb] = u32x4{0u, 0u, 0u, 0u};
     {
-      const rsrc_t dr = make_rsrc(a.deltaOut + row0 * OP, SEEDED ? 0 : (int64_t)vblk * 32 * OP);
-      const rsrc_t cr = make_rsrc(a.cOut + row0 * OP, (SEEDED && a.cOut) ? (int64_t)vblk * 64 * OP : 0);
-      const rsrc_t gr = make_rsrc(a.dY + row0 * out_dim, (SEEDED && a.dY) ? vrows * out_dim * 4 : 0);
+      const rsrc_t cr = make_rsrc(a.cOut + t.row0 * OP, (SEEDED && a.cOut) ? (int64_t)t.vblk * 64 * OP : 0);
+      const rsrc_t gr = make_rsrc(a.dY + t.row0 * out_dim, (SEEDED && a.dY) ? t.vrows * out_dim * 4 : 0);
       static_for<0, OS>([&](auto sc) {
         constexpr int s = decltype(sc)::value;
-        if (s >= SO) return;
         uint32_t p0, p1;
         if constexpr (!SEEDED) {
-          const u32x2 v = bload64(dr, lane * 8, (uint32_t)(s * 512));
-          p0 = v.x;
-          p1 = v.y;
+          p0 = dq[s].x;
+          p1 = dq[s].y;
         } else {
-          const int64_t m = row0 + li;
+          if (s >= SO) return;
+          const int64_t m = t.row0 + li;
           const int j0 = s * 16 + lg * 4;
           float g[4] = {0.f, 0.f, 0.f, 0.f};
           if (yvec) {
@@ -224,11 +260,13 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
         }
       });
     }
-    uint32_t mw = load_mask(L - 2);  // relu'(a_{L-1})
-    load_a(std::integral_constant<int, L - 1>{});
+    uint32_t mw = mq;  // relu'(a_{L-1})
 
-    // Layer l: D_{l+1} (in `cur`) into DT; D_l = (D_{l+1} W_l^T) relu'(a_l)
-    // into `nxt`; the wave's slice of G_l = A_l^T D_{l+1} over the tile.
+    // Layer l.  Phase 1: D_{l+1} (in `cur`) transposed into DT.  Phase 2
+    // (after a barrier): the wave's slice of G_l = A_l^T D_{l+1} over the
+    // tile, interleaved strip by strip with D_l = (D_{l+1} W_l^T) relu'(a_l)
+    // into `nxt` (independent work for the matrix cores while DT reads and
+    // weight reads are in flight).  A barrier then frees DT.
     auto layer_step = [&](auto lc, u32x4 (&cur)[KBW], u32x4 (&nxt)[KBW]) {
       constexpr int l = decltype(lc)::value;
       constexpr int SD = Gm::sd(l);
@@ -236,20 +274,58 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
         constexpr int s = decltype(sc)::value;
         const f32x4 o = mfma16(cur[s >> 1], (s & 1) ? sel1 : sel0, zero4);
         const u32x2 v = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-        // rows 4 g .. 4 g + 3 of block `wave`: positions 8 g + 4 (wave % 2)
-        // of contraction step wave / 2, so that a contraction operand is one
-        // 16-byte read holding the rows in the transposed A operand's order
-        *reinterpret_cast<u32x2*>(DT + (16 * s + li) * LDT + 32 * (wave >> 1) + 8 * lg + 4 * (wave & 1)) = v;
+        // rows 4 g .. 4 g + 3 of block `wave` go to chunk 4 (wave / 2) + g
+        // of feature row 16 s + n, half (wave % 2) ^ (g % 2): the order of
+        // the transposed A operand below
+        *reinterpret_cast<u32x2*>(DT + dt_off(16 * s + li, 4 * (wave >> 1) + lg) +
+                                  4 * ((wave & 1) ^ (lg & 1))) = v;
       });
-      if constexpr (l >= 1) {
-        constexpr int KBL = (l == L - 1) ? KBO : KBW;  // contraction over D_{l+1}'s features
-        const u32x4* wl = smem + (size_t)Gm::woff(l) * 64;
-        if constexpr (SW == 1) {
-          nxt[0].z = 0u;
-          nxt[0].w = 0u;
+      __syncthreads();  // DT holds D_{l+1} of all 128 rows
+
+      int kt, jt0;
+      const bool has = slice(lc, kt, jt0);
+      // A_l strip transposed: step ks holds rows 4 g + r of blocks 2 ks
+      // (slots r) and 2 ks + 1 (slots 4 + r), feature 16 kt + n in lane
+      // (g, n), the order the DT writes above used (odd lane groups hold
+      // block 2 ks + 1 in slots 0-3, see dt_off)
+      u32x4 aop[KS];
+      if (has) {
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) {
+          const u32x4 src = {ar[2 * ks].x, ar[2 * ks].y, ar[2 * ks + 1].x, ar[2 * ks + 1].y};
+          const f32x4 o0 = mfma16(src, sel0, zero4);
+          const f32x4 o1 = mfma16(src, sel1, zero4);
+          const uint32_t b00 = pack_bf16x2(o0[0], o0[1]), b01 = pack_bf16x2(o0[2], o0[3]);
+          const uint32_t b10 = pack_bf16x2(o1[0], o1[1]), b11 = pack_bf16x2(o1[2], o1[3]);
+          aop[ks] = (lg & 1) ? u32x4{b10, b11, b00, b01} : u32x4{b00, b01, b10, b11};
         }
-        static_for<0, SW>([&](auto sc) {
-          constexpr int s = decltype(sc)::value;
+      }
+      // ar is free: the next layer's strip, or the next tile's first inputs
+      if constexpr (l >= 1) {
+        load_a(std::integral_constant<int, l - 1>{}, t);
+      } else {
+        if (more) fetch(tile + G);
+      }
+      constexpr int TPW = Gm::tpw(l), GO = Gm::goff(l);
+      constexpr int NG = KS * TPW;              // G MFMAs of the slice
+      constexpr int NS = l >= 1 ? SW : 1;       // interleaving steps
+      constexpr int KBL = (l == L - 1) ? KBO : KBW;  // contraction over D_{l+1}'s features
+      const u32x4* wl = smem + (size_t)Gm::woff(l > 0 ? l : 1) * 64;
+      if constexpr (l >= 1 && SW == 1) {
+        nxt[0].z = 0u;
+        nxt[0].w = 0u;
+      }
+      static_for<0, NS>([&](auto sc) {
+        constexpr int s = decltype(sc)::value;
+        if (has) {
+          static_for<s * NG / NS, (s + 1) * NG / NS>([&](auto qc) {
+            constexpr int q = decltype(qc)::value;
+            constexpr int ks = q / TPW, u = q % TPW;
+            const u32x4 bop = *reinterpret_cast<const u32x4*>(DT + dt_off(16 * (jt0 + u) + li, 4 * ks + lg));
+            gacc[GO + u] = mfma16(aop[ks], bop, gacc[GO + u]);
+          });
+        }
+        if constexpr (l >= 1) {
           u32x4 af[KBL];
 #pragma unroll
           for (int kb = 0; kb < KBL; ++kb) af[kb] = wl[(s * KBL + kb) * 64 + lane];
@@ -257,9 +333,9 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
 #pragma unroll
           for (int kb = 0; kb < KBL; ++kb) acc = mfma16(af[kb], cur[kb], acc);
           // relu'(a) is [a > 0]: zero the rounded products where a is 0
-          const uint32_t t = mw >> (2 * s);
-          const uint32_t p0 = mask_halves(pack_bf16x2(acc[0], acc[1]), t & 0x00010001u);
-          const uint32_t p1 = mask_halves(pack_bf16x2(acc[2], acc[3]), (t >> 1) & 0x00010001u);
+          const uint32_t tm = mw >> (2 * s);
+          const uint32_t p0 = mask_halves(pack_bf16x2(acc[0], acc[1]), tm & 0x00010001u);
+          const uint32_t p1 = mask_halves(pack_bf16x2(acc[2], acc[3]), (tm >> 1) & 0x00010001u);
           if constexpr (s & 1) {
             nxt[s >> 1].z = p0;
             nxt[s >> 1].w = p1;
@@ -267,39 +343,10 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
             nxt[s >> 1].x = p0;
             nxt[s >> 1].y = p1;
           }
-          __builtin_amdgcn_sched_barrier(0);
-        });
-        if constexpr (l >= 2) mw = load_mask(l - 2);
-      }
-      __syncthreads();  // DT holds D_{l+1} of all 128 rows
-      int kt, jt0;
-      if (slice(lc, kt, jt0)) {
-        // A_l strip transposed: step ks holds rows 4 g + r of blocks 2 ks
-        // (slots r) and 2 ks + 1 (slots 4 + r), feature 16 kt + n in lane
-        // (g, n), the order the DT writes above used
-        u32x4 aop[KS];
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-          const u32x4 src = {ar[2 * ks].x, ar[2 * ks].y, ar[2 * ks + 1].x, ar[2 * ks + 1].y};
-          const f32x4 o0 = mfma16(src, sel0, zero4);
-          const f32x4 o1 = mfma16(src, sel1, zero4);
-          aop[ks] = u32x4{pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3]),
-                          pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
         }
-        if constexpr (l >= 1) load_a(std::integral_constant<int, l - 1>{});
-        constexpr int TPW = Gm::tpw(l), GO = Gm::goff(l);
-#pragma unroll
-        for (int ks = 0; ks < KS; ++ks) {
-#pragma unroll
-          for (int u = 0; u < TPW; ++u) {
-            const u32x4 bop =
-                *reinterpret_cast<const u32x4*>(DT + (16 * (jt0 + u) + li) * LDT + 32 * ks + 8 * lg);
-            gacc[GO + u] = mfma16(aop[ks], bop, gacc[GO + u]);
-          }
-        }
-      } else {
-        if constexpr (l >= 1) load_a(std::integral_constant<int, l - 1>{});
-      }
+        __builtin_amdgcn_sched_barrier(0);
+      });
+      if constexpr (l >= 2) mw = load_mask(l - 2, t);
       __syncthreads();  // every wave is done reading DT
     };
 
