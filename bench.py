@@ -14,7 +14,12 @@ against the dense bf16 MFMA peak.
 its algorithmic bytes per row.  `cpu_baseline` times the fp64 oracle on a
 bounded sample of the same step on the host cores.
 
-    python bench.py [--steps K] [--warmup W] [--width 128 --depth 4 --batch 1048576]
+    python bench.py [--steps K] [--warmup W] [--repeats R] [--width 128 --depth 4 --batch 1048576]
+    python bench.py --roofline-plot OUT.svg [--batch M] [--steps K --repeats R]
+
+The timing protocol of the paper's sweeps (section IV-A) is
+--steps max(1000 * 2^18 / M, 250) --warmup 10 --repeats 5: the median of
+five repeats, each the mean over the steps.
 """
 from __future__ import annotations
 
@@ -139,59 +144,36 @@ def cpu_baseline(width, depth, in_dim, out_dim, act, out_act, target_s=12.0):
             "value_1core": m1 / dt1, "sample_1core": f"{m1} rows, {dt1:.1f} s"}
 
 
-def main():
-    ap = argparse.ArgumentParser()
-    ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
-    ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--width", type=int, default=128)
-    ap.add_argument("--depth", type=int, default=4)
-    ap.add_argument("--in-dim", type=int, default=None)
-    ap.add_argument("--out-dim", type=int, default=16)
-    ap.add_argument("--batch", type=int, default=1 << 20)
-    ap.add_argument("--act", default="relu")
-    ap.add_argument("--out-act", default="linear")
-    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle timing")
-    ap.add_argument("--inputs", choices=["default", "cold", "hot"], default="default",
-                    help="default: X alternates between two buffers; cold: X and T rotate "
-                         "over at least 512 MiB of buffers (beyond the 256 MiB last-level "
-                         "cache); hot: one X and T buffer every step")
-    args = ap.parse_args()
-    if args.gpus != 1:
-        print("bench.py runs on one GPU only: the library has no multi-GPU path "
-              "(inference would shard rows with no communication; training would add "
-              "one all-reduce of the gradients).", file=sys.stderr)
-        sys.exit(2)
+def measure(width, depth, in_dim, out_dim, M, act, out_act, K, Wm, R=1, inputs="default"):
+    """Time K steps (after Wm warm-up steps) R times with HIP events on the
+    launch stream; returns the repeat with the median time per step, plus
+    the spread over the repeats."""
+    import statistics
 
     import torch
     import datagen
     import paper_2403_17607_amd as ffmlp
 
-    width, depth, M = args.width, args.depth, args.batch
-    in_dim = args.in_dim or width
-    out_dim = args.out_dim
     dev = torch.device("cuda:0")
-    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, args.act, args.out_act)
+    net = ffmlp.FusedMLP(width, depth, in_dim, out_dim, act, out_act)
     W = datagen.xavier_weights(2, width, depth, in_dim, out_dim, device=dev)
     # Input buffers used in turn.  By default two, so inference at large
     # batches does not run out of the 256 MiB last-level cache; "cold"
     # rotates X and T over at least 512 MiB whatever the batch, "hot" reuses
     # one of each.
-    if args.inputs == "cold":
+    if inputs == "cold":
         nbuf = max(2, -(-(512 << 20) // max(1, M * (2 * in_dim + 4 * out_dim))))
     else:
-        nbuf = 1 if args.inputs == "hot" else 2
+        nbuf = 1 if inputs == "hot" else 2
     Xs = [datagen.inputs_uniform(2 + i, M, in_dim, device=dev) for i in range(nbuf)]
     Ts = [datagen.targets_uniform(2 + i, M, out_dim, device=dev)
-          for i in range(nbuf if args.inputs == "cold" else 1)]
+          for i in range(nbuf if inputs == "cold" else 1)]
     packed = net.pack(W)
     ws = net.workspace(M, dev)
     Y = torch.empty(M, out_dim, dtype=torch.bfloat16, device=dev)
     G = torch.empty(net.param_count(), dtype=torch.float32, device=dev)
     loss = torch.empty(1, dtype=torch.float32, device=dev)
     stream = torch.cuda.current_stream(dev)
-
-    K, Wm = args.steps, args.warmup
     ev = [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in range(K)]
 
     def step(i, events=None):
@@ -215,27 +197,138 @@ def main():
     ref_copy = torch.empty_like(Xs[0])
     ref_copy.copy_(Xs[0])
     del ref_copy
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for i in range(K):
-        step(i, ev[i])
-    torch.cuda.synchronize()
-    wall = time.perf_counter() - t0
+    reps = []
+    for r in range(R):
+        torch.cuda.synchronize()
+        t0 = time.perf_counter()
+        for i in range(K):
+            step(i, ev[i])
+        torch.cuda.synchronize()
+        wall = time.perf_counter() - t0
+        reps.append({
+            "ms_per_step": wall * 1e3 / K,
+            "event_ms_per_step": sum(e[0].elapsed_time(e[3]) for e in ev) / K,
+            "infer_ms": sum(e[1].elapsed_time(e[2]) for e in ev) / K,
+            "train_ms": sum(e[2].elapsed_time(e[3]) for e in ev) / K,
+            "pack_ms": sum(e[0].elapsed_time(e[1]) for e in ev) / K,
+            "infer_ms_median_launch": statistics.median(e[1].elapsed_time(e[2]) for e in ev),
+        })
+    del ws
+    torch.cuda.empty_cache()
+    order = sorted(range(R), key=lambda r: reps[r]["ms_per_step"])
+    res = dict(reps[order[R // 2]])
+    res["repeats"] = R
+    if R > 1:
+        res["spread"] = {k: [min(x[k] for x in reps), max(x[k] for x in reps)]
+                         for k in ("ms_per_step", "infer_ms", "train_ms")}
+    res["nbuf"] = nbuf
+    return res
 
-    t_step = sum(e[0].elapsed_time(e[3]) for e in ev) / K  # ms
-    t_inf = sum(e[1].elapsed_time(e[2]) for e in ev) / K
-    t_train = sum(e[2].elapsed_time(e[3]) for e in ev) / K
-    t_pack = sum(e[0].elapsed_time(e[1]) for e in ev) / K
-    ms_per_step = wall * 1e3 / K
 
+def summarize(width, depth, in_dim, out_dim, M, act, out_act, m):
+    """Derived rates of one measurement: samples/s, algorithmic TFLOP/s and
+    HBM GB/s of the inference launch and of the training step."""
     fl_inf, fl_train = flops_per_row(width, depth, in_dim, out_dim)
-    fused = fused_backward(width, depth, in_dim, out_dim, args.act)
-    inf_tflops = fl_inf * M / (t_inf * 1e-3) / 1e12
-    train_tflops = fl_train * M / (t_train * 1e-3) / 1e12
-    bytes_inf = M * (2 * in_dim + 2 * out_dim)
-    bytes_train = M * train_bytes_per_row(width, depth, in_dim, out_dim, args.act)
-    train_gbs = bytes_train / (t_train * 1e-3) / 1e9
+    t_inf, t_train = m["infer_ms"], m["train_ms"]
+    bytes_inf = 2 * in_dim + 2 * out_dim
+    bytes_train = train_bytes_per_row(width, depth, in_dim, out_dim, act)
+    return {
+        "infer": {"ms": t_inf, "samples_per_s": M / (t_inf * 1e-3),
+                  "tflops": fl_inf * M / (t_inf * 1e-3) / 1e12,
+                  "pct_bf16_peak": 100 * fl_inf * M / (t_inf * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                  "hbm_gbs_algorithmic": bytes_inf * M / (t_inf * 1e-3) / 1e9,
+                  "flop_per_byte": fl_inf / bytes_inf},
+        "train": {"ms": t_train, "samples_per_s": M / (t_train * 1e-3),
+                  "tflops": fl_train * M / (t_train * 1e-3) / 1e12,
+                  "pct_bf16_peak": 100 * fl_train * M / (t_train * 1e-3) / 1e12 / PEAK_BF16_TFLOPS,
+                  "hbm_gbs_algorithmic": bytes_train * M / (t_train * 1e-3) / 1e9,
+                  "flop_per_byte": fl_train / bytes_train, "bytes_per_row": bytes_train},
+    }
 
+
+def roofline_plot(path, points, batch):
+    """Arithmetic intensity against achieved TFLOP/s, with the HBM and MFMA
+    roofs, one point per width for inference and for the training step."""
+    import matplotlib
+    matplotlib.use("Agg")
+    matplotlib.rcParams["svg.fonttype"] = "none"  # text as text: a small SVG
+    import matplotlib.pyplot as plt
+    ai = [2 ** (k / 8) for k in range(0, 8 * 12 + 1)]  # 1 .. 4096 flop/B
+    fig, ax = plt.subplots(figsize=(7.5, 5))
+    ax.plot(ai, [min(PEAK_BF16_TFLOPS, PEAK_HBM_GBS * a / 1e3) for a in ai], "k-", lw=1.5,
+            label="MI355X roofline (8 TB/s HBM, 2.5 PFLOP/s dense bf16)")
+    for kind, marker in (("infer", "o"), ("train", "s")):
+        xs = [p[kind]["flop_per_byte"] for p in points]
+        ys = [p[kind]["tflops"] for p in points]
+        ax.plot(xs, ys, marker, ms=7, label={"infer": "inference (Algorithm 1)",
+                                             "train": "training step (Algorithm 2)"}[kind])
+        for p, x, y in zip(points, xs, ys):
+            ax.annotate(f"w{p['width']}", (x, y), textcoords="offset points", xytext=(5, -10),
+                        fontsize=8)
+    ax.set_xscale("log", base=2)
+    ax.set_yscale("log", base=10)
+    ax.set_xlabel("algorithmic arithmetic intensity (flop / HBM byte)")
+    ax.set_ylabel("achieved TFLOP/s (algorithmic flops)")
+    ax.set_title(f"Fused MLP, 4 hidden layers, in = width, out 16, ReLU, batch {batch}")
+    ax.grid(True, which="both", lw=0.3)
+    ax.legend(fontsize=8, loc="lower right")
+    fig.tight_layout()
+    fig.savefig(path, metadata={"Date": None})
+    plt.close(fig)
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--repeats", type=int, default=1,
+                    help="time the K steps this many times and report the median repeat "
+                         "(with the min-max spread)")
+    ap.add_argument("--width", type=int, default=128)
+    ap.add_argument("--depth", type=int, default=4)
+    ap.add_argument("--in-dim", type=int, default=None)
+    ap.add_argument("--out-dim", type=int, default=16)
+    ap.add_argument("--batch", type=int, default=1 << 20)
+    ap.add_argument("--act", default="relu")
+    ap.add_argument("--out-act", default="linear")
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle timing")
+    ap.add_argument("--inputs", choices=["default", "cold", "hot"], default="default",
+                    help="default: X alternates between two buffers; cold: X and T rotate "
+                         "over at least 512 MiB of buffers (beyond the 256 MiB last-level "
+                         "cache); hot: one X and T buffer every step")
+    ap.add_argument("--roofline-plot", metavar="SVG",
+                    help="instead of the bench line: measure widths 16, 32, 64, 128 (in = "
+                         "width, out 16, 4 hidden layers, ReLU) at --batch and draw arithmetic "
+                         "intensity against achieved TFLOP/s under the roofs")
+    args = ap.parse_args()
+    if args.gpus != 1:
+        print("bench.py runs on one GPU only: the library has no multi-GPU path "
+              "(inference would shard rows with no communication; training would add "
+              "one all-reduce of the gradients).", file=sys.stderr)
+        sys.exit(2)
+
+    K, Wm, R, M = args.steps, args.warmup, args.repeats, args.batch
+    if args.roofline_plot:
+        points = []
+        for w in (16, 32, 64, 128):
+            m = measure(w, 4, w, 16, M, "relu", "linear", K, Wm, R)
+            p = summarize(w, 4, w, 16, M, "relu", "linear", m)
+            p["width"] = w
+            points.append(p)
+            print(json.dumps({"width": w, "batch": M, **p}), flush=True)
+        roofline_plot(args.roofline_plot, points, M)
+        return
+
+    width, depth = args.width, args.depth
+    in_dim = args.in_dim or width
+    out_dim = args.out_dim
+    m = measure(width, depth, in_dim, out_dim, M, args.act, args.out_act, K, Wm, R, args.inputs)
+    d = summarize(width, depth, in_dim, out_dim, M, args.act, args.out_act, m)
+    fused = fused_backward(width, depth, in_dim, out_dim, args.act)
+    fl_inf, _ = flops_per_row(width, depth, in_dim, out_dim)
+    inf_tflops, train_gbs = d["infer"]["tflops"], d["train"]["hbm_gbs_algorithmic"]
+    ms_per_step = m["ms_per_step"]
     out = {
         "metric": METRIC,
         "value": M / (ms_per_step * 1e-3),
@@ -255,25 +348,24 @@ def main():
                    "width": width, "depth": depth, "in_dim": in_dim, "out_dim": out_dim,
                    "batch": M, "activation": args.act, "output_activation": args.out_act,
                    "inputs": {"default": "X alternates between 2 buffers",
-                              "cold": f"X and T rotate over {nbuf} buffers (>= 512 MiB)",
+                              "cold": f"X and T rotate over {m['nbuf']} buffers (>= 512 MiB)",
                               "hot": "one X and T buffer"}[args.inputs]},
-        "infer": {"ms": t_inf, "samples_per_s": M / (t_inf * 1e-3), "tflops": inf_tflops,
-                  "pct_bf16_peak": 100 * inf_tflops / PEAK_BF16_TFLOPS,
-                  "hbm_gbs_algorithmic": bytes_inf / (t_inf * 1e-3) / 1e9},
-        "train": {"ms": t_train, "samples_per_s": M / (t_train * 1e-3), "tflops": train_tflops,
-                  "pct_bf16_peak": 100 * train_tflops / PEAK_BF16_TFLOPS,
-                  "hbm_gbs_algorithmic": train_gbs},
-        "pack_ms": t_pack,
-        "event_ms_per_step": t_step,
+        **d,
+        "pack_ms": m["pack_ms"],
+        "event_ms_per_step": m["event_ms_per_step"],
+        "repeats": R,
         "roofline": {"kernel": "fwd_kernel (inference)", "bound": "mfma",
                      "achieved": inf_tflops, "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
                      "frac": inf_tflops / PEAK_BF16_TFLOPS,
-                     "launch_us": t_inf * 1e3,
+                     "launch_us": m["infer_ms"] * 1e3,
+                     "launch_us_median": m["infer_ms_median_launch"] * 1e3,
                      "traffic": measured_traffic(
                          f"fwd_infer_w{width}_d{depth}_in{in_dim}_out{out_dim}_{args.act}_b{M}")
                      if args.out_act == "linear" else None,
-                     "traffic_unit": "HBM bytes per launch (rocprofv3 FETCH_SIZE + WRITE_SIZE, "
-                                     "scaled by a reference copy)",
+                     "traffic_unit": "HBM bytes per launch: a committed rocprofv3 "
+                                     "FETCH_SIZE + WRITE_SIZE measurement of this kernel and "
+                                     "workload (profiles/traffic.json, scaled by a reference "
+                                     "copy), null once the kernel's sources have changed",
                      "flops_per_row": fl_inf, "rows_per_launch": M},
         "roofline_train": {"kernels": ("fwd_kernel (train) + bwdg_kernel (fused backward and "
                                        "weight gradients) + reduce_kernel") if fused else
@@ -290,8 +382,8 @@ def main():
                                width, depth, in_dim, out_dim, args.act, fused=False,
                                masks=False)},
     }
-    del ws
-    torch.cuda.empty_cache()
+    if R > 1:
+        out["spread"] = m["spread"]
     if not args.no_cpu:
         out["cpu_baseline"] = cpu_baseline(width, depth, in_dim, out_dim, args.act, args.out_act)
     print(json.dumps(out), flush=True)
