@@ -56,14 +56,30 @@ __device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], const u32x
 // us, width 64 at 2^17 rows 12.6 -> 11.0 us); every other case uses the
 // tile configuration.  The row tile changes with it; the stash layout
 // does not.
-template <int W, int MODE, bool SMALL = false>
+// Width-128 inference runs two 16-row blocks per wave and 16 waves per
+// workgroup (4 per SIMD instead of 2 with four blocks and 8 waves: more
+// waves to hide the latencies of the layer transitions and the X loads;
+// the fragment reads per row double, a quarter of LDS bandwidth at the full
+// MFMA rate).  Measured at 2^20 rows: 5 matrices 112.1 -> 106.5 us, depth 16
+// with streamed weights 494.6 -> 474.1 us.  The even-L fused loop (FU 2)
+// needs more registers than the 128 that 4 waves per SIMD leave and runs 12
+// waves (97.7 -> 93.5 us for 4 matrices).
+template <int W, int MODE, bool SMALL = false, int FU = 0>
 constexpr int fwd_waves() {
+  if constexpr (W == 128 && MODE == FWD_INFER && !SMALL) return FU == 2 ? 12 : 16;
   return ((W <= 32 || SMALL) && MODE == FWD_INFER) ? 8 : TileCfg<W>::NW;
+}
+// 16-row blocks per wave.
+template <int W, int MODE, bool SMALL = false, int FU = 0>
+constexpr int fwd_nt() {
+  if constexpr (SMALL) return 1;
+  if constexpr (W == 128 && MODE == FWD_INFER) return 2;
+  return TileCfg<W>::NT;
 }
 
 template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false>
-__global__ __launch_bounds__((fwd_waves<W, MODE, SMALL>() * 64)) void fwd_kernel(const FwdArgs a) {
-  constexpr int NT = SMALL ? 1 : TileCfg<W>::NT, NW = fwd_waves<W, MODE, SMALL>();
+__global__ __launch_bounds__((fwd_waves<W, MODE, SMALL, FU>() * 64)) void fwd_kernel(const FwdArgs a) {
+  constexpr int NT = fwd_nt<W, MODE, SMALL, FU>(), NW = fwd_waves<W, MODE, SMALL, FU>();
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
   extern __shared__ u32x4 smem[];
   const int tid = threadIdx.x, lane = tid & 63;
@@ -522,14 +538,21 @@ __global__ __launch_bounds__((fwd_waves<W, MODE, SMALL>() * 64)) void fwd_kernel
   }
 }
 
+// A kernel instantiation with its block size and row tile.
+struct FwdPick {
+  void (*kern)(FwdArgs);
+  int threads;
+  int64_t rows;
+};
+template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false>
+static FwdPick fwd_pick() {
+  constexpr int NW = fwd_waves<W, MODE, SMALL, FU>(), NT = fwd_nt<W, MODE, SMALL, FU>();
+  return FwdPick{fwd_kernel<W, ACT, MODE, FU, RES, SMALL>, NW * 64, (int64_t)NW * NT * 16};
+}
+
 template <int W, int ACT, int MODE>
 static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out) {
-  int NTH = fwd_waves<W, MODE>() * 64;
   FwdArgs a = a0;
-  if constexpr (fwd_waves<W, MODE>() != TileCfg<W>::NW) {
-    const int64_t rows = (int64_t)TileCfg<W>::NT * fwd_waves<W, MODE>() * 16;
-    a.ntiles = (int)((a.M + rows - 1) / rows);
-  }
   DeviceInfo di;
   hipError_t e = device_info(&di);
   if (e != hipSuccess) return e;
@@ -543,36 +566,32 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
   // (1297 against 1334 us for the whole step), so it keeps 1 KiB spare.
   a.resident = res_bytes + (MODE == FWD_INFER ? 0 : 1024) <= (size_t)di.max_lds ? 1 : 0;
   const size_t lds = a.resident ? res_bytes : (size_t)2 * maxf * 1024;
-  void (*kern)(FwdArgs) =
-      a.resident ? fwd_kernel<W, ACT, MODE, 0, true> : fwd_kernel<W, ACT, MODE, 0, false>;
+  FwdPick pk = a.resident ? fwd_pick<W, ACT, MODE, 0, true>() : fwd_pick<W, ACT, MODE, 0, false>();
   if constexpr (MODE == FWD_INFER && W >= 64) {
     if (a.resident && a.L >= 2 && SO == 1 && (a.in_dim % 8) == 0)
-      kern = (a.L & 1) ? fwd_kernel<W, ACT, MODE, 1, true> : fwd_kernel<W, ACT, MODE, 2, true>;
+      pk = (a.L & 1) ? fwd_pick<W, ACT, MODE, 1, true>() : fwd_pick<W, ACT, MODE, 2, true>();
     else if (a.L >= 2 && (a.in_dim % 8) == 0)
-      kern = a.resident ? ((a.L & 1) ? fwd_kernel<W, ACT, MODE, 4, true> : fwd_kernel<W, ACT, MODE, 3, true>)
-                        : ((a.L & 1) ? fwd_kernel<W, ACT, MODE, 4, false> : fwd_kernel<W, ACT, MODE, 3, false>);
+      pk = a.resident ? ((a.L & 1) ? fwd_pick<W, ACT, MODE, 4, true>() : fwd_pick<W, ACT, MODE, 3, true>())
+                      : ((a.L & 1) ? fwd_pick<W, ACT, MODE, 4, false>() : fwd_pick<W, ACT, MODE, 3, false>());
   }
   if constexpr (MODE == FWD_INFER && W <= 64) {
     // Small batches: fewer than two row tiles of the tile configuration
     // (NT NW 16 rows) per CU (widths up to 64, whose weights leave LDS for
     // several workgroups per CU).
     const int64_t cfg_rows = (int64_t)TileCfg<W>::NT * TileCfg<W>::NW * 16;
-    if ((a.M + cfg_rows - 1) / cfg_rows <= 2 * (int64_t)di.cus && a.resident) {
-      kern = fwd_kernel<W, ACT, MODE, 0, true, true>;
-      NTH = fwd_waves<W, MODE, true>() * 64;
-      const int64_t rows = (int64_t)fwd_waves<W, MODE, true>() * 16;
-      a.ntiles = (int)((a.M + rows - 1) / rows);
-    }
+    if ((a.M + cfg_rows - 1) / cfg_rows <= 2 * (int64_t)di.cus && a.resident)
+      pk = fwd_pick<W, ACT, MODE, 0, true, true>();
   }
+  a.ntiles = (int)((a.M + pk.rows - 1) / pk.rows);
   int occ = 0;
-  e = kernel_occupancy(reinterpret_cast<const void*>(kern), NTH, lds, &occ);
+  e = kernel_occupancy(reinterpret_cast<const void*>(pk.kern), pk.threads, lds, &occ);
   if (e != hipSuccess) return e;
   int grid = di.cus * occ;
   if (grid > a.ntiles) grid = a.ntiles;
   if (grid > kMaxLossParts) grid = kMaxLossParts;
   if (grid < 1) grid = 1;
   if (grid_out) *grid_out = grid;
-  hipLaunchKernelGGL(kern, dim3(grid), dim3(NTH), lds, stream, a);
+  hipLaunchKernelGGL(pk.kern, dim3(grid), dim3(pk.threads), lds, stream, a);
   return hipGetLastError();
 }
 
