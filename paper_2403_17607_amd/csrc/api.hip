@@ -210,6 +210,7 @@ int run_fused_backward(const mlp* h, const void* packed, const uint16_t* X, cons
   a.X = X;
   a.stashA = reinterpret_cast<const uint16_t*>(ws + w.stashA);
   a.reluMask = reinterpret_cast<const uint32_t*>(ws + w.reluMask);
+  a.stashS = h->act == MLP_ACT_SINE ? reinterpret_cast<const uint16_t*>(ws + w.stashS) : nullptr;
   a.deltaOut = reinterpret_cast<const uint16_t*>(ws + w.deltaOut);
   a.cOut = h->out_act != MLP_ACT_LINEAR ? reinterpret_cast<const float*>(ws + w.cOut) : nullptr;
   a.dY = dY;
@@ -219,6 +220,7 @@ int run_fused_backward(const mlp* h, const void* packed, const uint16_t* X, cons
   a.params = param_count(h);
   a.in_dim = h->in_dim;
   a.out_dim = h->out_dim;
+  a.act = h->act;
   a.out_act = h->out_act;
   a.ntiles = (int)((M + kBwdgRows - 1) / kBwdgRows);
   a.layH_frags = g.bwd_hidden;

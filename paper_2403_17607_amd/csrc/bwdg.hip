@@ -6,10 +6,10 @@
 namespace ffmlp {
 
 bool backward_fused_supported(int width, int L, int act, int in_dim, int out_dim) {
-  if (act != ACT_RELU || L < 2 || L > kBwdgMaxL) return false;
-  if (in_dim % 4 != 0) return false;  // X is read 4 features (8 bytes) per lane
-  if (width == 128 && out_dim > 16) return false;
-  return width == 16 || width == 32 || width == 64 || width == 128;
+  (void)in_dim;
+  if (L < 2 || L > kBwdgMaxL) return false;
+  if (width == 128) return act == ACT_RELU && out_dim <= 16;  // register budget
+  return width == 16 || width == 32 || width == 64;
 }
 
 hipError_t launch_backward_fused(int width, int L, int out_dim, int seeded, const BwdgArgs& a,

@@ -8,7 +8,7 @@ template <>
 hipError_t launch_backward_fused_w<32>(int L, int out_dim, int seeded, const BwdgArgs& a,
                                         hipStream_t s, int* grid_out) {
   (void)out_dim;
-  return bwdg_by_l<32, 2>(L, seeded, a, s, grid_out);
+  return bwdg_by_act<32, 2>(L, seeded, a, s, grid_out);
 }
 
 }  // namespace ffmlp

@@ -2,7 +2,12 @@
 // Algorithm 2, D_i = sigma_b(A_i, D_{i+1} B_i^T), and the products
 // G_i = A_i^T D_{i+1} in one kernel (arXiv 2403.17607, section III-A; the
 // paper computes G outside its fused kernel and names fusing it into the
-// backward pass as future work in section V).  ReLU hidden layers.
+// backward pass as future work in section V).
+//
+// The hidden activations' derivative comes, for ReLU nets (DER = 0), from
+// the mask words the forward pass wrote; otherwise (DER = 1, widths up to
+// 64) from the stash: bf16 cos C for sine, A (1 - A) of the stored bf16 A
+// for sigmoid, 1 for linear.
 //
 // A workgroup of eight waves owns a tile of 128 batch rows at a time
 // (persistent loop over tiles).  Each wave carries the deltas of its own 16
@@ -59,7 +64,7 @@ struct BwdgGeom {
   static_assert(L >= 2 && L <= kBwdgMaxL, "fused backward: 2 .. kBwdgMaxL matrices");
 };
 
-template <int W, int L, int OS, int SEEDED>
+template <int W, int L, int OS, int SEEDED, int DER>
 __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a) {
   using Gm = BwdgGeom<W, L, OS>;
   constexpr int NW = Gm::NW, SW = Gm::SW, KBW = Gm::KBW, KBO = Gm::KBO, LDT = Gm::LDT;
@@ -71,7 +76,8 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int li = lane & 15, lg = lane >> 4;
   const int64_t M = a.M;
-  const int in_dim = a.in_dim, out_dim = a.out_dim, out_act = a.out_act;
+  const int in_dim = a.in_dim, out_dim = a.out_dim, act = a.act, out_act = a.out_act;
+  const bool xvec = (in_dim & 3) == 0;
   const int SO = (out_dim + 15) >> 4;  // strips of the output (at most OS)
   const int OP = SO * 16;
   const bool yvec = (out_dim & 3) == 0;
@@ -172,9 +178,24 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
       rows = rows < 0 ? 0 : (rows > kBwdgRows ? kBwdgRows : rows);
       const rsrc_t xr = make_rsrc(a.X + t.tr0 * in_dim, rows * in_dim * 2);
       const int f0 = 16 * kt + 4 * lg;
-      const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
+      if (xvec) {
+        // in_dim a multiple of 4: the lane's four features in one 8-byte load
+        const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
 #pragma unroll
-      for (int b = 0; b < NW; ++b) ar[b] = bload64(xr, voff, (uint32_t)(b * 32 * in_dim));
+        for (int b = 0; b < NW; ++b) ar[b] = bload64(xr, voff, (uint32_t)(b * 32 * in_dim));
+      } else {
+        // other input widths: one 2-byte load per feature (zero past in_dim)
+        uint32_t vo[4];
+#pragma unroll
+        for (int r = 0; r < 4; ++r) vo[r] = f0 + r < in_dim ? (uint32_t)((li * in_dim + f0 + r) * 2) : kOOB;
+#pragma unroll
+        for (int b = 0; b < NW; ++b) {
+          uint32_t e[4];
+#pragma unroll
+          for (int r = 0; r < 4; ++r) e[r] = bload16(xr, vo[r], (uint32_t)(b * 32 * in_dim));
+          ar[b] = u32x2{e[0] | (e[1] << 16), e[2] | (e[3] << 16)};
+        }
+      }
     } else {
       const rsrc_t sr = make_rsrc(a.stashA + (size_t)(l - 1) * a.M16 * W + (size_t)t.tr0 * W,
                                   (int64_t)t.tvblk * 32 * W);
@@ -187,11 +208,30 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
                                 t.vblk ? 256 : 0);
     return bload32(mr, lane * 4, 0u);
   };
+  // DER = 1: the derivative source of hidden activation idx (stash index),
+  // the wave's own 16 rows, all strips (none for linear layers).
+  auto load_der = [&](int idx, const TileGeom& t, u32x2 (&sv)[SW]) {
+    if (act == ACT_LINEAR) return;
+    const uint16_t* src = act == ACT_SINE ? a.stashS : a.stashA;
+    const rsrc_t r = make_rsrc(src + (size_t)idx * a.M16 * W + (size_t)t.row0 * W,
+                               (int64_t)t.vblk * 32 * W);
+#pragma unroll
+    for (int s = 0; s < SW; ++s) sv[s] = bload64(r, lane * 8, (uint32_t)(s * 512));
+  };
+  // relu'(a) of the derivative source values as a factor: sigmoid a (1 - a)
+  // of the stored bf16 a, sine the stored bf16 cos c, linear 1.
+  auto der = [&](uint32_t half) -> float {
+    const float v = __uint_as_float(half);
+    return act == ACT_SIGMOID ? v * (1.f - v) : (act == ACT_SINE ? v : 1.f);
+  };
   // What a tile needs first, requested one tile ahead (during the previous
   // tile's last layer): the output delta (training mode), the mask words of
   // a_{L-1} and the A strip of layer L-1.
   u32x2 dq[OS];
   uint32_t mq = 0u;
+  u32x2 svq[DER ? SW : 1], sv[DER ? SW : 1];  // derivative sources (DER = 1)
+#pragma unroll
+  for (int s = 0; s < (DER ? SW : 1); ++s) svq[s] = sv[s] = u32x2{0u, 0u};
   auto fetch = [&](int tile) {
     const TileGeom t = geom(tile);
     if constexpr (!SEEDED) {
@@ -200,7 +240,8 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
       for (int s = 0; s < OS; ++s)
         dq[s] = bload64(dr, lane * 8, s < SO ? (uint32_t)(s * 512) : kOOB);
     }
-    mq = load_mask(L - 2, t);
+    if constexpr (DER == 0) mq = load_mask(L - 2, t);
+    else load_der(L - 2, t, svq);
     load_a(std::integral_constant<int, L - 1>{}, t);
   };
 
@@ -261,6 +302,10 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
       });
     }
     uint32_t mw = mq;  // relu'(a_{L-1})
+    if constexpr (DER == 1) {
+#pragma unroll
+      for (int s = 0; s < SW; ++s) sv[s] = svq[s];
+    }
 
     // Layer l.  Phase 1: D_{l+1} (in `cur`) transposed into DT.  Phase 2
     // (after a barrier): the wave's slice of G_l = A_l^T D_{l+1} over the
@@ -332,10 +377,16 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
           f32x4 acc = zero4;
 #pragma unroll
           for (int kb = 0; kb < KBL; ++kb) acc = mfma16(af[kb], cur[kb], acc);
-          // relu'(a) is [a > 0]: zero the rounded products where a is 0
-          const uint32_t tm = mw >> (2 * s);
-          const uint32_t p0 = mask_halves(pack_bf16x2(acc[0], acc[1]), tm & 0x00010001u);
-          const uint32_t p1 = mask_halves(pack_bf16x2(acc[2], acc[3]), (tm >> 1) & 0x00010001u);
+          uint32_t p0, p1;
+          if constexpr (DER == 0) {
+            // relu'(a) is [a > 0]: zero the rounded products where a is 0
+            const uint32_t tm = mw >> (2 * s);
+            p0 = mask_halves(pack_bf16x2(acc[0], acc[1]), tm & 0x00010001u);
+            p1 = mask_halves(pack_bf16x2(acc[2], acc[3]), (tm >> 1) & 0x00010001u);
+          } else {
+            p0 = pack_bf16x2(acc[0] * der(sv[s].x << 16), acc[1] * der(sv[s].x & 0xffff0000u));
+            p1 = pack_bf16x2(acc[2] * der(sv[s].y << 16), acc[3] * der(sv[s].y & 0xffff0000u));
+          }
           if constexpr (s & 1) {
             nxt[s >> 1].z = p0;
             nxt[s >> 1].w = p1;
@@ -346,7 +397,10 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
         }
         __builtin_amdgcn_sched_barrier(0);
       });
-      if constexpr (l >= 2) mw = load_mask(l - 2, t);
+      if constexpr (l >= 2) {
+        if constexpr (DER == 0) mw = load_mask(l - 2, t);
+        else load_der(l - 2, t, sv);
+      }
       __syncthreads();  // every wave is done reading DT
     };
 
@@ -381,7 +435,7 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
   });
 }
 
-template <int W, int L, int OS, int SEEDED>
+template <int W, int L, int OS, int SEEDED, int DER>
 static hipError_t bwdg_launch_t(const BwdgArgs& a, hipStream_t stream, int* grid_out) {
   using Gm = BwdgGeom<W, L, OS>;
   DeviceInfo di;
@@ -389,7 +443,7 @@ static hipError_t bwdg_launch_t(const BwdgArgs& a, hipStream_t stream, int* grid
   if (e != hipSuccess) return e;
   const size_t lds = Gm::lds_bytes();
   if (lds > (size_t)di.max_lds) return hipErrorNotSupported;
-  auto kern = bwdg_kernel<W, L, OS, SEEDED>;
+  auto kern = bwdg_kernel<W, L, OS, SEEDED, DER>;
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), kBwdgWaves * 64, lds, &occ);
   if (e != hipSuccess) return e;
@@ -402,24 +456,23 @@ static hipError_t bwdg_launch_t(const BwdgArgs& a, hipStream_t stream, int* grid
   return hipGetLastError();
 }
 
-template <int W, int OS>
+template <int W, int OS, int DER>
 static hipError_t bwdg_by_l(int L, int seeded, const BwdgArgs& a, hipStream_t s, int* g) {
   switch (L) {
-    case 2: return seeded ? bwdg_launch_t<W, 2, OS, 1>(a, s, g) : bwdg_launch_t<W, 2, OS, 0>(a, s, g);
-    case 3: return seeded ? bwdg_launch_t<W, 3, OS, 1>(a, s, g) : bwdg_launch_t<W, 3, OS, 0>(a, s, g);
-    case 4: return seeded ? bwdg_launch_t<W, 4, OS, 1>(a, s, g) : bwdg_launch_t<W, 4, OS, 0>(a, s, g);
-    case 5: return seeded ? bwdg_launch_t<W, 5, OS, 1>(a, s, g) : bwdg_launch_t<W, 5, OS, 0>(a, s, g);
+    case 2: return seeded ? bwdg_launch_t<W, 2, OS, 1, DER>(a, s, g) : bwdg_launch_t<W, 2, OS, 0, DER>(a, s, g);
+    case 3: return seeded ? bwdg_launch_t<W, 3, OS, 1, DER>(a, s, g) : bwdg_launch_t<W, 3, OS, 0, DER>(a, s, g);
+    case 4: return seeded ? bwdg_launch_t<W, 4, OS, 1, DER>(a, s, g) : bwdg_launch_t<W, 4, OS, 0, DER>(a, s, g);
+    case 5: return seeded ? bwdg_launch_t<W, 5, OS, 1, DER>(a, s, g) : bwdg_launch_t<W, 5, OS, 0, DER>(a, s, g);
     default: return hipErrorNotSupported;
   }
 }
-
-// Output-strip classes compiled per width: the kernel's register slices of
-// the output layer's G are sized for OS strips.
-template <int W>
-constexpr int bwdg_os(int out_dim) {
-  if constexpr (W == 128) return out_dim <= 16 ? 1 : 0;  // 0: not compiled
-  else if constexpr (W == 64) return out_dim <= 16 ? 1 : 4;
-  else return W / 16;
+// ReLU nets read the mask words (DER 0); widths up to 64 also cover the
+// other hidden activations from the stash (DER 1).
+template <int W, int OS>
+static hipError_t bwdg_by_act(int L, int seeded, const BwdgArgs& a, hipStream_t s, int* g) {
+  if (a.act == ACT_RELU) return bwdg_by_l<W, OS, 0>(L, seeded, a, s, g);
+  if constexpr (W <= 64) return bwdg_by_l<W, OS, 1>(L, seeded, a, s, g);
+  return hipErrorNotSupported;
 }
 
 template <int W>

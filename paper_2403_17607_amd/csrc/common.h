@@ -142,13 +142,14 @@ struct BwdgArgs {
   const u32x4* packed;       // backward-packed weights, layers 1 .. L-1
   const uint16_t* X;         // [M][in_dim]
   const uint16_t* stashA;    // (L-1) x [M16][W] tile images: a_1 .. a_{L-1}
-  const uint32_t* reluMask;  // (L-1) x [M16/16][64] ReLU mask words
+  const uint32_t* reluMask;  // (L-1) x [M16/16][64] ReLU mask words (ReLU nets)
+  const uint16_t* stashS;    // (L-1) x [M16][W] bf16 cos of sine layers, or null
   const uint16_t* deltaOut;  // [M16][OP] output delta (training step)
   const float* cOut;         // [M16][OP] fp32 pre-activation (seeded, nonlinear output)
   const float* dY;           // [M][out_dim] (seeded mode)
   float* partial;            // [gridDim.x][params]
   int64_t M, M16, params;
-  int in_dim, out_dim, out_act;
+  int in_dim, out_dim, act, out_act;
   int ntiles;                // kBwdgRows-row tiles
   uint32_t layH_frags;       // 1 KiB fragments of one packed hidden layer
 };

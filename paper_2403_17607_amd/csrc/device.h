@@ -126,6 +126,9 @@ __device__ __forceinline__ u32x4 bload128(rsrc_t r, uint32_t voff, uint32_t soff
 __device__ __forceinline__ uint32_t bload32(rsrc_t r, uint32_t voff, uint32_t soff) {
   return __builtin_amdgcn_raw_buffer_load_b32(r, voff, soff, 0);
 }
+__device__ __forceinline__ uint32_t bload16(rsrc_t r, uint32_t voff, uint32_t soff) {
+  return (uint32_t)__builtin_amdgcn_raw_buffer_load_b16(r, voff, soff, 0);
+}
 // Stores are non-temporal (cache policy nt) by default: everything the
 // forward and backward kernels store (outputs, the activation and delta
 // stash, masks, dX) is read at most once, by a later kernel, so keeping it

@@ -47,9 +47,9 @@ __device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], const u32x
 // the register allocation of one loop does not constrain another and no
 // loop carries the other's branches (whose joins force conservative waits
 // on LDS loads).
-// SMALL: one 16-row block per wave (inference on batches that give the
-// usual tiles fewer than two per compute unit, widths up to 64): four
-// times as many workgroups, so more waves share each CU's latency.
+// SMALL: one 16-row block per wave (batches that give the usual tiles
+// fewer than two per compute unit, widths up to 64): four times as many
+// workgroups, so more waves share each CU's latency.
 // Waves per workgroup: inference at widths up to 32, and the small-batch
 // variant at any width, stream X and Y with little arithmetic per byte and
 // run 8 waves (more bytes in flight per CU: width 16 at 2^22 rows 66 -> 56
@@ -67,7 +67,7 @@ __device__ __forceinline__ void strip_product(const u32x4 (&af)[KBW], const u32x
 template <int W, int MODE, bool SMALL = false, int FU = 0>
 constexpr int fwd_waves() {
   if constexpr (W == 128 && MODE == FWD_INFER && !SMALL) return FU == 2 ? 12 : 16;
-  return ((W <= 32 || SMALL) && MODE == FWD_INFER) ? 8 : TileCfg<W>::NW;
+  return (SMALL || (W <= 32 && MODE == FWD_INFER)) ? 8 : TileCfg<W>::NW;
 }
 // 16-row blocks per wave.
 template <int W, int MODE, bool SMALL = false, int FU = 0>
@@ -574,10 +574,10 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
       pk = a.resident ? ((a.L & 1) ? fwd_pick<W, ACT, MODE, 4, true>() : fwd_pick<W, ACT, MODE, 3, true>())
                       : ((a.L & 1) ? fwd_pick<W, ACT, MODE, 4, false>() : fwd_pick<W, ACT, MODE, 3, false>());
   }
-  if constexpr (MODE == FWD_INFER && W <= 64) {
+  if constexpr (W <= 64) {
     // Small batches: fewer than two row tiles of the tile configuration
     // (NT NW 16 rows) per CU (widths up to 64, whose weights leave LDS for
-    // several workgroups per CU).
+    // several workgroups per CU), inference and training forward alike.
     const int64_t cfg_rows = (int64_t)TileCfg<W>::NT * TileCfg<W>::NW * 16;
     if ((a.M + cfg_rows - 1) / cfg_rows <= 2 * (int64_t)di.cus && a.resident)
       pk = fwd_pick<W, ACT, MODE, 0, true, true>();
