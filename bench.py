@@ -50,18 +50,18 @@ def flops_per_row(width, depth, in_dim, out_dim):
 def fused_backward(width, depth, in_dim, out_dim, act):
     """Whether the library's training step runs the fused backward kernel
     (deltas kept on chip, weight gradients accumulated in the same kernel):
-    ReLU hidden layers, 2 to 5 weight matrices, in_dim a multiple of 4 and,
-    at width 128, at most 16 outputs; otherwise it runs the three kernels
-    (backward, weight gradients, reduce).  The rule of include/ffmlp.h."""
-    return (act == "relu" and 1 <= depth <= 4 and in_dim % 4 == 0
-            and (width != 128 or out_dim <= 16))
+    2 to 5 weight matrices and, at width 128, ReLU hidden layers and at most
+    16 outputs; otherwise it runs the three kernels (backward, weight
+    gradients, reduce).  The rule of include/ffmlp.h."""
+    return 1 <= depth <= 4 and (width != 128 or (act == "relu" and out_dim <= 16))
 
 
 def train_bytes_per_row(width, depth, in_dim, out_dim, act, fused=None, masks=True):
     """HBM bytes the training step must move per row.
     Forward (both plans): reads X and T, writes the activations, the output
     delta and (ReLU) the activation masks.
-    Fused plan: the backward kernel reads the output delta, the masks, X and
+    Fused plan: the backward kernel reads the output delta, the derivative
+    source of every hidden activation (as in the three-kernel plan), X and
     the activations (the weight-gradient operands) and writes no deltas.
     Three-kernel plan: the backward reads the output delta and the
     derivative source of every hidden activation (ReLU: its mask, 16 B per
@@ -79,7 +79,7 @@ def train_bytes_per_row(width, depth, in_dim, out_dim, act, fused=None, masks=Tr
     if act == "sine":
         b += hid                                          # cos stash write
     if fused:
-        return b + 2 * OP + mask + 2 * in_dim + hid       # fused backward
+        return b + 2 * OP + deriv + 2 * in_dim + hid      # fused backward
     b += 2 * OP + deriv + hid                             # backward
     b += 2 * in_dim + hid + hid + 2 * OP                  # weight gradients
     return b

@@ -164,11 +164,11 @@ int mlp_backward_dx(const mlp_t* h, const void* packed, const uint16_t* X,
  *   loss  optional device float, set to sum (Y - T)^2 / (M out_dim)
  *         computed from the fp32 outputs before rounding.
  *   ws    mlp_workspace_bytes(h, M, MLP_MODE_TRAIN) bytes, 256-byte aligned.
- * Kernels: the forward pass, then for ReLU nets of 2 to 5 weight matrices
- * with in_dim a multiple of 4 (and out_dim <= 16 at width 128) one fused
- * kernel that propagates the deltas and accumulates the weight gradients
- * without storing the deltas (the fusion section V of the paper proposes),
- * otherwise a backward kernel and a weight-gradient kernel; then a
+ * Kernels: the forward pass, then for nets of 2 to 5 weight matrices (at
+ * width 128 only ReLU nets with out_dim <= 16) one fused kernel that
+ * propagates the deltas and accumulates the weight gradients without
+ * storing the deltas (the fusion section V of the paper proposes), for
+ * other nets a backward kernel and a weight-gradient kernel; then a
  * fixed-order reduction, so G is bitwise the same from run to run.
  * mlp_backward uses the same rule; mlp_backward_dx always the latter.
  */
