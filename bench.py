@@ -60,9 +60,10 @@ def train_bytes_per_row(width, depth, in_dim, out_dim, act, fused=None, masks=Tr
     """HBM bytes the training step must move per row.
     Forward (both plans): reads X and T, writes the activations, the output
     delta and (ReLU) the activation masks.
-    Fused plan: the backward kernel reads the output delta, the derivative
-    source of every hidden activation (as in the three-kernel plan), X and
-    the activations (the weight-gradient operands) and writes no deltas.
+    Fused plan: the backward kernel reads the output delta, X and the
+    activations (the weight-gradient operands; at widths up to 64 also the
+    ReLU and sigmoid derivative source), plus the masks at width 128 and the
+    cos stash of sine nets, and writes no deltas.
     Three-kernel plan: the backward reads the output delta and the
     derivative source of every hidden activation (ReLU: its mask, 16 B per
     row, or with masks=False the activation itself; sigmoid: the
@@ -73,13 +74,19 @@ def train_bytes_per_row(width, depth, in_dim, out_dim, act, fused=None, masks=Tr
         fused = fused_backward(width, depth, in_dim, out_dim, act)
     OP = (out_dim + 15) // 16 * 16
     hid = depth * width * 2
+    if fused:
+        # ReLU masks only at width 128; at widths up to 64 the fused kernel
+        # takes relu' (and sigmoid's a (1 - a)) from the activations it reads
+        # for the weight gradients: one read of them
+        mask = depth * 16 if (act == "relu" and width == 128) else 0
+        cos = hid if act == "sine" else 0
+        b = 2 * in_dim + 4 * out_dim + hid + 2 * OP + mask + cos   # forward (train)
+        return b + 2 * OP + mask + cos + 2 * in_dim + hid           # fused backward
     mask = depth * 16 if (act == "relu" and masks) else 0
     deriv = {"relu": mask if masks else hid, "linear": 0}.get(act, hid)
     b = 2 * in_dim + 4 * out_dim + hid + 2 * OP + mask    # forward (train)
     if act == "sine":
         b += hid                                          # cos stash write
-    if fused:
-        return b + 2 * OP + deriv + 2 * in_dim + hid      # fused backward
     b += 2 * OP + deriv + hid                             # backward
     b += 2 * in_dim + hid + hid + 2 * OP                  # weight gradients
     return b

@@ -201,7 +201,7 @@ int run_reduce(const mlp* h, const WsLayout& w, uint8_t* ws, int64_t M, int P, f
 // Returns 1 (nothing enqueued) when the fused kernel does not cover the net.
 int run_fused_backward(const mlp* h, const void* packed, const uint16_t* X, const float* dY,
                        const WsLayout& w, uint8_t* ws, int64_t M, float* G, float* loss, int nloss,
-                       int seeded, hipStream_t s) {
+                       int seeded, bool masks, hipStream_t s) {
   if (M <= 0 || !backward_fused_supported(h->width, n_mats(h), h->act, h->in_dim, h->out_dim))
     return 1;
   const PackGeom g = pack_geom(h);
@@ -209,7 +209,8 @@ int run_fused_backward(const mlp* h, const void* packed, const uint16_t* X, cons
   a.packed = reinterpret_cast<const u32x4*>(static_cast<const uint8_t*>(packed) + (size_t)g.fwd_total * 1024);
   a.X = X;
   a.stashA = reinterpret_cast<const uint16_t*>(ws + w.stashA);
-  a.reluMask = reinterpret_cast<const uint32_t*>(ws + w.reluMask);
+  a.reluMask = (h->act == MLP_ACT_RELU && masks) ? reinterpret_cast<const uint32_t*>(ws + w.reluMask)
+                                                 : nullptr;
   a.stashS = h->act == MLP_ACT_SINE ? reinterpret_cast<const uint16_t*>(ws + w.stashS) : nullptr;
   a.deltaOut = reinterpret_cast<const uint16_t*>(ws + w.deltaOut);
   a.cOut = h->out_act != MLP_ACT_LINEAR ? reinterpret_cast<const float*>(ws + w.cOut) : nullptr;
@@ -544,7 +545,7 @@ int mlp_backward_dx(const mlp_t* h, const void* packed, const uint16_t* X, const
   const WsLayout w = ws_layout(h, M);
   uint8_t* ws = static_cast<uint8_t*>(ws_);
   if (!dX && n_mats(h) > 1) {
-    const int rc = run_fused_backward(h, packed, X, dY, w, ws, M, G, nullptr, 0, 1, s);
+    const int rc = run_fused_backward(h, packed, X, dY, w, ws, M, G, nullptr, 0, 1, true, s);
     if (rc <= 0) return rc;
   }
   if (M > 0) {
@@ -606,14 +607,22 @@ int train_step_impl(const mlp_t* h, const void* packed, const uint16_t* X, const
     a.T = T;
     a.stashA = reinterpret_cast<uint16_t*>(ws + w.stashA);
     a.stashS = h->act == MLP_ACT_SINE ? reinterpret_cast<uint16_t*>(ws + w.stashS) : nullptr;
-    a.reluMask = h->act == MLP_ACT_RELU ? reinterpret_cast<uint32_t*>(ws + w.reluMask) : nullptr;
+    // The fused backward at widths up to 64 reads relu' from the stashed
+    // activations (which it reads for the weight gradients anyway), so the
+    // training forward writes no mask words for it.
+    const bool fused = n_mats(h) > 1 &&
+                       backward_fused_supported(h->width, n_mats(h), h->act, h->in_dim, h->out_dim);
+    const bool masks = h->act == MLP_ACT_RELU && !(fused && h->width <= 64);
+    a.reluMask = masks ? reinterpret_cast<uint32_t*>(ws + w.reluMask) : nullptr;
     a.deltaOut = reinterpret_cast<uint16_t*>(ws + w.deltaOut);
     a.lossPart = reinterpret_cast<float*>(ws + w.lossPart);
     hipError_t e = launch_forward(h->width, h->act, FWD_TRAIN, a, s, &nloss);
     if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
     if (n_mats(h) > 1) {
-      const int rc = run_fused_backward(h, packed, X, nullptr, w, ws, M, G, loss, nloss, 0, s);
+      const int rc = run_fused_backward(h, packed, X, nullptr, w, ws, M, G, loss, nloss, 0, masks, s);
       if (rc <= 0) return rc;
+      if (h->act == MLP_ACT_RELU && !masks)  // the unfused backward needs the masks
+        return fail(MLP_ERR_UNSUPPORTED, "fused backward kernel unavailable on this device");
       BwdArgs b = bwd_args(h, packed, w, ws, M);
       e = launch_backward(h->width, h->act, 0, b, s);
       if (e != hipSuccess) return hip_fail(e, "backward kernel launch");

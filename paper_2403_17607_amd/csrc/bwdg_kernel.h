@@ -4,10 +4,11 @@
 // paper computes G outside its fused kernel and names fusing it into the
 // backward pass as future work in section V).
 //
-// The hidden activations' derivative comes, for ReLU nets (DER = 0), from
-// the mask words the forward pass wrote; otherwise (DER = 1, widths up to
-// 64) from the stash: bf16 cos C for sine, A (1 - A) of the stored bf16 A
-// for sigmoid, 1 for linear.
+// The hidden activations' derivative comes from the mask words the forward
+// pass wrote (DER 0: ReLU nets with masks), or, at widths up to 64, from the
+// stash: [A > 0] for ReLU (DER 1) and A (1 - A) for sigmoid (DER 2) from the
+// stored bf16 A (the rows of A this CU reads for its G slices anyway, so
+// mostly cache hits), bf16 cos C for sine and 1 for linear (DER 2).
 //
 // A workgroup of eight waves owns a tile of 128 batch rows at a time
 // (persistent loop over tiles).  Each wave carries the deltas of its own 16
@@ -218,8 +219,9 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
 #pragma unroll
     for (int s = 0; s < SW; ++s) sv[s] = bload64(r, lane * 8, (uint32_t)(s * 512));
   };
-  // relu'(a) of the derivative source values as a factor: sigmoid a (1 - a)
-  // of the stored bf16 a, sine the stored bf16 cos c, linear 1.
+  // The derivative of the hidden activation from its source value (DER 2):
+  // sigmoid a (1 - a) of the stored bf16 a, sine the stored bf16 cos c,
+  // linear 1.
   auto der = [&](uint32_t half) -> float {
     const float v = __uint_as_float(half);
     return act == ACT_SIGMOID ? v * (1.f - v) : (act == ACT_SINE ? v : 1.f);
@@ -229,7 +231,7 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
   // a_{L-1} and the A strip of layer L-1.
   u32x2 dq[OS];
   uint32_t mq = 0u;
-  u32x2 svq[DER ? SW : 1], sv[DER ? SW : 1];  // derivative sources (DER = 1)
+  u32x2 svq[DER ? SW : 1], sv[DER ? SW : 1];  // derivative sources (DER 1, 2)
 #pragma unroll
   for (int s = 0; s < (DER ? SW : 1); ++s) svq[s] = sv[s] = u32x2{0u, 0u};
   auto fetch = [&](int tile) {
@@ -302,7 +304,7 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
       });
     }
     uint32_t mw = mq;  // relu'(a_{L-1})
-    if constexpr (DER == 1) {
+    if constexpr (DER != 0) {
 #pragma unroll
       for (int s = 0; s < SW; ++s) sv[s] = svq[s];
     }
@@ -383,6 +385,11 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
             const uint32_t tm = mw >> (2 * s);
             p0 = mask_halves(pack_bf16x2(acc[0], acc[1]), tm & 0x00010001u);
             p1 = mask_halves(pack_bf16x2(acc[2], acc[3]), (tm >> 1) & 0x00010001u);
+          } else if constexpr (DER == 1) {
+            // ReLU from the stored activations: each bf16 half of a is >= 0,
+            // so its 0/1 multiplier is min(a, 1) as an unsigned 16-bit value
+            p0 = mask_halves(pack_bf16x2(acc[0], acc[1]), nonzero_halves(sv[s].x));
+            p1 = mask_halves(pack_bf16x2(acc[2], acc[3]), nonzero_halves(sv[s].y));
           } else {
             p0 = pack_bf16x2(acc[0] * der(sv[s].x << 16), acc[1] * der(sv[s].x & 0xffff0000u));
             p1 = pack_bf16x2(acc[2] * der(sv[s].y << 16), acc[3] * der(sv[s].y & 0xffff0000u));
@@ -466,12 +473,15 @@ static hipError_t bwdg_by_l(int L, int seeded, const BwdgArgs& a, hipStream_t s,
     default: return hipErrorNotSupported;
   }
 }
-// ReLU nets read the mask words (DER 0); widths up to 64 also cover the
-// other hidden activations from the stash (DER 1).
+// ReLU nets with mask words read them (DER 0); widths up to 64 also take
+// the derivative from the stash (DER 1 for ReLU, 2 for the others).
 template <int W, int OS>
 static hipError_t bwdg_by_act(int L, int seeded, const BwdgArgs& a, hipStream_t s, int* g) {
-  if (a.act == ACT_RELU) return bwdg_by_l<W, OS, 0>(L, seeded, a, s, g);
-  if constexpr (W <= 64) return bwdg_by_l<W, OS, 1>(L, seeded, a, s, g);
+  if (a.act == ACT_RELU && a.reluMask) return bwdg_by_l<W, OS, 0>(L, seeded, a, s, g);
+  if constexpr (W <= 64) {
+    if (a.act == ACT_RELU) return bwdg_by_l<W, OS, 1>(L, seeded, a, s, g);
+    return bwdg_by_l<W, OS, 2>(L, seeded, a, s, g);
+  }
   return hipErrorNotSupported;
 }
 

@@ -40,18 +40,20 @@ def test_training_bytes_per_row():
 
 
 def test_fused_training_bytes_per_row():
-    """Fused plan: 4 in + 4 out + 4 d W + 4 OP, plus the ReLU masks written
-    and read (2 16 d) or the sine cos stash (4 d W): no hidden delta is
-    written or read."""
-    fused = lambda w, d, i, o: 4 * i + 4 * o + 4 * d * w + 4 * ((o + 15) // 16 * 16) + 32 * d
+    """Fused plan: 4 in + 4 out + 4 d W + 4 OP, plus at width 128 the ReLU
+    masks written and read (2 16 d), or for sine the cos stash (4 d W): no
+    hidden delta is written or read."""
+    fused = lambda w, d, i, o: 4 * i + 4 * o + 4 * d * w + 4 * ((o + 15) // 16 * 16)
     assert bench.fused_backward(128, 4, 128, 16, "relu")
-    assert bench.train_bytes_per_row(128, 4, 128, 16, "relu") == fused(128, 4, 128, 16) == 2816
-    assert bench.train_bytes_per_row(16, 4, 16, 16, "relu") == fused(16, 4, 16, 16) == 576
+    # width 128: the ReLU masks written and read (2 16 d)
+    assert bench.train_bytes_per_row(128, 4, 128, 16, "relu") == fused(128, 4, 128, 16) + 128 == 2816
+    # widths up to 64: relu' from the activations, no masks
+    assert bench.train_bytes_per_row(16, 4, 16, 16, "relu") == fused(16, 4, 16, 16) == 448
     assert bench.train_bytes_per_row(64, 2, 64, 3, "relu") == fused(64, 2, 64, 3)
-    # sine: the cos stash written and read again, no masks
+    assert bench.train_bytes_per_row(64, 2, 64, 3, "sigmoid") == fused(64, 2, 64, 3)
+    # sine: the cos stash written and read again
     hid = 4 * 64 * 2
-    assert bench.train_bytes_per_row(64, 4, 3, 1, "sine") == \
-        (2 * 3 + 4 * 1 + hid + 2 * 16 + hid) + (2 * 16 + hid + 2 * 3 + hid)
+    assert bench.train_bytes_per_row(64, 4, 3, 1, "sine") == fused(64, 4, 3, 1) + 2 * hid
     # outside the fused kernel's nets: the three-kernel count
     for args in [(128, 4, 128, 128, "relu"), (128, 16, 128, 128, "relu"), (128, 4, 128, 16, "sine"),
                  (64, 5, 64, 16, "sigmoid"), (64, 0, 64, 16, "relu")]:
