@@ -1,6 +1,7 @@
-// Fused backward kernel instantiations for width 32 (the kernel is in
-// bwdg_kernel.h).
+// Fused backward kernel instantiations for width 32: the per-wave variant
+// (bwdn_kernel.h), which keeps every layer's whole G in each wave.
 #include "bwdg_kernel.h"
+#include "bwdn_kernel.h"
 
 namespace ffmlp {
 
@@ -8,7 +9,7 @@ template <>
 hipError_t launch_backward_fused_w<32>(int L, int out_dim, int seeded, const BwdgArgs& a,
                                         hipStream_t s, int* grid_out) {
   (void)out_dim;
-  return bwdg_by_act<32, 2>(L, seeded, a, s, grid_out);
+  return bwdn_by_act<32, 2>(L, seeded, a, s, grid_out);
 }
 
 }  // namespace ffmlp

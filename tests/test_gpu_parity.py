@@ -523,24 +523,27 @@ def test_train_step_full_batch(ffmlp, gpu, width, depth, in_dim, out_dim, M):
     assert lerr <= LOSS_TOL
 
 
-@pytest.mark.parametrize("width,depth,in_dim,out_dim,out_act", [
-    (128, 1, 128, 16, "linear"), (128, 2, 100, 3, "sigmoid"), (128, 3, 128, 16, "relu"),
-    (128, 4, 64, 1, "linear"),
-    (64, 1, 32, 16, "linear"), (64, 2, 64, 3, "sigmoid"), (64, 3, 60, 64, "linear"),
-    (64, 4, 64, 40, "sine"),
-    (32, 1, 8, 32, "linear"), (32, 4, 32, 17, "sigmoid"),
-    (16, 2, 16, 5, "linear"), (16, 4, 12, 16, "relu"),
+@pytest.mark.parametrize("width,depth,in_dim,out_dim,act,out_act", [
+    (128, 1, 128, 16, "relu", "linear"), (128, 2, 100, 3, "relu", "sigmoid"),
+    (128, 3, 128, 16, "relu", "relu"), (128, 4, 64, 1, "relu", "linear"),
+    (64, 1, 32, 16, "relu", "linear"), (64, 2, 64, 3, "relu", "sigmoid"),
+    (64, 3, 60, 64, "relu", "linear"), (64, 4, 64, 40, "relu", "sine"),
+    (32, 1, 8, 32, "relu", "linear"), (32, 4, 32, 17, "relu", "sigmoid"),
+    (32, 4, 30, 32, "sine", "linear"), (32, 2, 32, 1, "sigmoid", "sigmoid"),
+    (16, 2, 16, 5, "relu", "linear"), (16, 4, 12, 16, "relu", "relu"),
+    (16, 3, 7, 16, "sine", "sine"), (16, 1, 16, 16, "linear", "relu"),
 ])
-def test_fused_backward_shapes(ffmlp, gpu, width, depth, in_dim, out_dim, out_act):
-    """ReLU nets of 2 to 5 matrices take the fused backward kernel (deltas
-    kept on chip, weight-gradient slices in registers): every width, both
-    output-strip classes at width 64, input widths that are multiples of 4
-    but not of 16, every output activation, and a batch of several 128-row
-    tiles per workgroup with a ragged tail.  The training step and the
-    seeded backward (after a stashing forward) against the oracle."""
+def test_fused_backward_shapes(ffmlp, gpu, width, depth, in_dim, out_dim, act, out_act):
+    """Nets of 2 to 5 matrices take the fused backward kernel (deltas kept
+    on chip, weight gradients in registers): every width, both output-strip
+    classes at width 64, input widths that are multiples of 4 and ones that
+    are not (7, 30), every hidden activation at the narrow widths, every
+    output activation, and a batch of several tiles per workgroup with a
+    ragged tail.  The training step and the seeded backward (after a
+    stashing forward) against the oracle."""
     M = 70001
-    log(f"fused w={width} d={depth} in={in_dim} out={out_dim} out_act={out_act} M={M}")
-    r = run_case(ffmlp, gpu, width, depth, in_dim, out_dim, M, "relu", out_act, seed=40 + depth)
+    log(f"fused w={width} d={depth} in={in_dim} out={out_dim} act={act} out_act={out_act} M={M}")
+    r = run_case(ffmlp, gpu, width, depth, in_dim, out_dim, M, act, out_act, seed=40 + depth)
     net, onet, packed, W, X = r["net"], r["onet"], r["packed"], r["W"], r["X"]
     dY = datagen.uniform(41, datagen.STREAM_AUX, (M, out_dim))
     ws = r["ws"]
