@@ -56,8 +56,17 @@ def fused_backward(width, depth, in_dim, out_dim, act):
     return 1 <= depth <= 4 and (width != 128 or (act == "relu" and out_dim <= 16))
 
 
+def fused_step(width, depth):
+    """Whether the library runs the whole training step as one kernel
+    (widths 16 and 32, 2 to 5 weight matrices): the activations stay in
+    registers, so only X and T (and Y when asked for) touch HBM."""
+    return width in (16, 32) and 1 <= depth <= 4
+
+
 def train_bytes_per_row(width, depth, in_dim, out_dim, act, fused=None, masks=True):
     """HBM bytes the training step must move per row.
+    One-kernel step (fused=None at widths 16 and 32 with 2 to 5 matrices):
+    X and T (the bench asks for no Y).
     Forward (both plans): reads X and T, writes the activations, the output
     delta and (ReLU) the activation masks.
     Fused plan: the backward kernel reads the output delta, X and the
@@ -71,6 +80,8 @@ def train_bytes_per_row(width, depth, in_dim, out_dim, act, fused=None, masks=Tr
     deltas; the gradient kernel reads X, the activations, the hidden deltas
     and the output delta."""
     if fused is None:
+        if fused_step(width, depth):
+            return 2 * in_dim + 4 * out_dim
         fused = fused_backward(width, depth, in_dim, out_dim, act)
     OP = (out_dim + 15) // 16 * 16
     hid = depth * width * 2
@@ -374,10 +385,14 @@ def main():
                                      "workload (profiles/traffic.json, scaled by a reference "
                                      "copy), null once the kernel's sources have changed",
                      "flops_per_row": fl_inf, "rows_per_launch": M},
-        "roofline_train": {"kernels": ("fwd_kernel (train) + bwdg_kernel (fused backward and "
-                                       "weight gradients) + reduce_kernel") if fused else
-                                      ("fwd_kernel (train) + bwd_kernel + wgrad_kernel + "
-                                       "reduce_kernel"),
+        "roofline_train": {"kernels": ("trainf_kernel (the whole step) + reduce_kernel"
+                                       if fused_step(width, depth) else
+                                       ("fwd_kernel (train) + " +
+                                        ("bwdn_kernel" if width <= 32 else "bwdg_kernel") +
+                                        " (fused backward and weight gradients) + reduce_kernel")
+                                       if fused else
+                                       ("fwd_kernel (train) + bwd_kernel + wgrad_kernel + "
+                                        "reduce_kernel")),
                            "bound": "hbm", "achieved": train_gbs,
                            "peak": PEAK_HBM_GBS, "unit": "GB/s",
                            "frac": train_gbs / PEAK_HBM_GBS,

@@ -164,13 +164,17 @@ int mlp_backward_dx(const mlp_t* h, const void* packed, const uint16_t* X,
  *   loss  optional device float, set to sum (Y - T)^2 / (M out_dim)
  *         computed from the fp32 outputs before rounding.
  *   ws    mlp_workspace_bytes(h, M, MLP_MODE_TRAIN) bytes, 256-byte aligned.
- * Kernels: the forward pass, then for nets of 2 to 5 weight matrices (at
- * width 128 only ReLU nets with out_dim <= 16) one fused kernel that
- * propagates the deltas and accumulates the weight gradients without
- * storing the deltas (the fusion section V of the paper proposes), for
- * other nets a backward kernel and a weight-gradient kernel; then a
- * fixed-order reduction, so G is bitwise the same from run to run.
- * mlp_backward uses the same rule; mlp_backward_dx always the latter.
+ * Kernels: at widths 16 and 32 with 2 to 5 weight matrices, one kernel for
+ * the whole step (forward, loss, backward and weight gradients, the hidden
+ * activations kept in registers: only X, T and Y touch memory).  Otherwise
+ * the forward pass, then for nets of 2 to 5 weight matrices (at width 128
+ * only ReLU nets with out_dim <= 16) one fused kernel that propagates the
+ * deltas and accumulates the weight gradients without storing the deltas
+ * (the fusion section V of the paper proposes), for other nets a backward
+ * kernel and a weight-gradient kernel.  Then a fixed-order reduction, so G
+ * and the loss are bitwise the same from run to run.  mlp_backward uses
+ * the same rule for its backward kernels; mlp_backward_dx always the
+ * unfused pair.
  */
 int mlp_train_step(const mlp_t* h, const void* packed, const uint16_t* X,
                    const float* T, uint16_t* Y, float* G, float* loss,

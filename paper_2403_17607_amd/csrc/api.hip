@@ -601,6 +601,29 @@ int train_step_impl(const mlp_t* h, const void* packed, const uint16_t* X, const
   const WsLayout w = ws_layout(h, M);
   uint8_t* ws = static_cast<uint8_t*>(ws_);
   int nloss = 0;
+  if (M > 0 && train_fused_supported(h->width, n_mats(h))) {
+    // Widths 16 and 32: the whole step in one kernel, then the reduce.
+    const PackGeom g = pack_geom(h);
+    TrainfArgs t{};
+    t.packedF = static_cast<const u32x4*>(packed);
+    t.packedB = reinterpret_cast<const u32x4*>(static_cast<const uint8_t*>(packed) + (size_t)g.fwd_total * 1024);
+    t.X = X;
+    t.T = T;
+    t.Y = Y;
+    t.partial = reinterpret_cast<float*>(ws + w.partial);
+    t.lossPart = reinterpret_cast<float*>(ws + w.lossPart);
+    t.M = M;
+    t.params = param_count(h);
+    t.in_dim = h->in_dim;
+    t.out_dim = h->out_dim;
+    t.out_act = h->out_act;
+    t.scale = (float)(2.0 / ((double)M * h->out_dim));
+    t.fwd_total = g.fwd_total;
+    int P = 0;
+    hipError_t e = launch_train_fused(h->width, n_mats(h), h->act, h->out_dim, t, s, &P);
+    if (e == hipSuccess) return run_reduce(h, w, ws, M, P, G, loss, P, s);
+    if (e != hipErrorNotSupported) return hip_fail(e, "fused training kernel launch");
+  }
   if (M > 0) {
     FwdArgs a = fwd_args(h, packed, X, M);
     a.Y = Y;

@@ -154,6 +154,26 @@ struct BwdgArgs {
   uint32_t layH_frags;       // 1 KiB fragments of one packed hidden layer
 };
 
+// Fused training step (trainf_kernel): the forward pass, the loss, the
+// backward pass and the weight gradients of nets of width 16 and 32 in one
+// kernel; the hidden activations stay in registers.
+constexpr int kTrainfWaves = 8;  // waves per workgroup
+constexpr int kTrainfMaxL = 5;   // weight matrices of the largest net
+struct TrainfArgs {
+  const u32x4* packedF;  // forward-packed weights, layers 0 .. L-1
+  const u32x4* packedB;  // backward-packed weights, layers 1 .. L-1
+  const uint16_t* X;     // [M][in_dim]
+  const float* T;        // [M][out_dim]
+  uint16_t* Y;           // [M][out_dim] or null
+  float* partial;        // [gridDim.x][params]
+  float* lossPart;       // [gridDim.x]
+  int64_t M, params;
+  int in_dim, out_dim, out_act;
+  float scale;           // 2 / (M out_dim)
+  int ntiles;            // set by the launcher
+  uint32_t fwd_total;    // 1 KiB fragments of the forward-packed layers
+};
+
 struct WgradArgs {
   const uint16_t* X;
   const uint16_t* stashA;
@@ -213,6 +233,12 @@ hipError_t launch_backward_fused(int width, int L, int out_dim, int seeded, cons
                                  hipStream_t s, int* grid_out);
 // Whether launch_backward_fused covers a net (host-side shape check only).
 bool backward_fused_supported(int width, int L, int act, int in_dim, int out_dim);
+// Fused training step; *grid_out receives the number of G and loss
+// partials written.  hipErrorNotSupported when it does not cover the net.
+hipError_t launch_train_fused(int width, int L, int act, int out_dim, const TrainfArgs& a,
+                              hipStream_t s, int* grid_out);
+// Whether launch_train_fused covers a net (host-side shape check only).
+bool train_fused_supported(int width, int L);
 hipError_t launch_reduce(const ReduceArgs& a, hipStream_t s);
 hipError_t launch_pack(const PackArgs& a, hipStream_t s);
 hipError_t launch_optim(const OptArgs& a, hipStream_t s);

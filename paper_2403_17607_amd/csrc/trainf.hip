@@ -1,0 +1,26 @@
+// Fused training step entry: which nets it covers, and dispatch on the
+// width; each width's instantiations are compiled in their own translation
+// unit (trainf16.hip, trainf32.hip), the kernel itself is in trainf_kernel.h.
+#include "trainf_kernel.h"
+
+namespace ffmlp {
+
+template <int W>
+hipError_t launch_train_fused_w(int L, int act, int out_dim, const TrainfArgs& a, hipStream_t s,
+                                int* grid_out);
+
+bool train_fused_supported(int width, int L) {
+  return (width == 16 || width == 32) && L >= 2 && L <= kTrainfMaxL;
+}
+
+hipError_t launch_train_fused(int width, int L, int act, int out_dim, const TrainfArgs& a,
+                              hipStream_t s, int* grid_out) {
+  if (!train_fused_supported(width, L)) return hipErrorNotSupported;
+  switch (width) {
+    case 16: return launch_train_fused_w<16>(L, act, out_dim, a, s, grid_out);
+    case 32: return launch_train_fused_w<32>(L, act, out_dim, a, s, grid_out);
+    default: return hipErrorNotSupported;
+  }
+}
+
+}  // namespace ffmlp

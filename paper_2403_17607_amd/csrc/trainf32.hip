@@ -1,0 +1,18 @@
+// Fused training step instantiations for width 32 (the kernel is in
+// trainf_kernel.h); out_dim <= 32, so at most 2 output strip(s).
+#include "trainf_kernel.h"
+
+namespace ffmlp {
+
+template <int W>
+hipError_t launch_train_fused_w(int L, int act, int out_dim, const TrainfArgs& a, hipStream_t s,
+                                int* grid_out);
+
+template <>
+hipError_t launch_train_fused_w<32>(int L, int act, int out_dim, const TrainfArgs& a, hipStream_t s,
+                                    int* grid_out) {
+  (void)out_dim;
+  return trainf_by_act<32, 2>(act, L, a, s, grid_out);
+}
+
+}  // namespace ffmlp
