@@ -58,14 +58,14 @@ def fused_backward(width, depth, in_dim, out_dim, act):
 
 def fused_step(width, depth):
     """Whether the library runs the whole training step as one kernel
-    (widths 16 and 32, 2 to 5 weight matrices): the activations stay in
-    registers, so only X and T (and Y when asked for) touch HBM."""
-    return width in (16, 32) and 1 <= depth <= 4
+    (widths 16, 32 and 64, 2 to 5 weight matrices): the activations stay on
+    chip, so only X and T (and Y when asked for) touch HBM."""
+    return width in (16, 32, 64) and 1 <= depth <= 4
 
 
 def train_bytes_per_row(width, depth, in_dim, out_dim, act, fused=None, masks=True):
     """HBM bytes the training step must move per row.
-    One-kernel step (fused=None at widths 16 and 32 with 2 to 5 matrices):
+    One-kernel step (fused=None at widths 16, 32 and 64 with 2 to 5 matrices):
     X and T (the bench asks for no Y).
     Forward (both plans): reads X and T, writes the activations, the output
     delta and (ReLU) the activation masks.
@@ -385,7 +385,8 @@ def main():
                                      "workload (profiles/traffic.json, scaled by a reference "
                                      "copy), null once the kernel's sources have changed",
                      "flops_per_row": fl_inf, "rows_per_launch": M},
-        "roofline_train": {"kernels": ("trainf_kernel (the whole step) + reduce_kernel"
+        "roofline_train": {"kernels": (("trainw_kernel" if width == 64 else "trainf_kernel") +
+                                       " (the whole step) + reduce_kernel"
                                        if fused_step(width, depth) else
                                        ("fwd_kernel (train) + " +
                                         ("bwdn_kernel" if width <= 32 else "bwdg_kernel") +

@@ -164,9 +164,9 @@ int mlp_backward_dx(const mlp_t* h, const void* packed, const uint16_t* X,
  *   loss  optional device float, set to sum (Y - T)^2 / (M out_dim)
  *         computed from the fp32 outputs before rounding.
  *   ws    mlp_workspace_bytes(h, M, MLP_MODE_TRAIN) bytes, 256-byte aligned.
- * Kernels: at widths 16 and 32 with 2 to 5 weight matrices, one kernel for
- * the whole step (forward, loss, backward and weight gradients, the hidden
- * activations kept in registers: only X, T and Y touch memory).  Otherwise
+ * Kernels: at widths 16, 32 and 64 with 2 to 5 weight matrices, one kernel
+ * for the whole step (forward, loss, backward and weight gradients, the
+ * hidden activations kept on chip: only X, T and Y touch memory).  Otherwise
  * the forward pass, then for nets of 2 to 5 weight matrices (at width 128
  * only ReLU nets with out_dim <= 16) one fused kernel that propagates the
  * deltas and accumulates the weight gradients without storing the deltas

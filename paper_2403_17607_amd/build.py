@@ -21,7 +21,7 @@ LIB = os.path.join(PKG, "libffmlp.so")
 SOURCES = ["api.hip", "fwd.hip", "fwd16.hip", "fwd32.hip", "fwd64.hip", "fwd128.hip",
            "bwd.hip", "bwd16.hip", "bwd32.hip", "bwd64.hip", "bwd128.hip",
            "bwdg.hip", "bwdg16.hip", "bwdg32.hip", "bwdg64.hip", "bwdg128.hip",
-           "trainf.hip", "trainf16.hip", "trainf32.hip", "wgrad.hip", "optim.hip"]
+           "trainf.hip", "trainf16.hip", "trainf32.hip", "trainf64.hip", "wgrad.hip", "optim.hip"]
 ARCH = "gfx950"
 
 HIPCC = shutil.which("hipcc") or "/opt/rocm/bin/hipcc"

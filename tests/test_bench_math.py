@@ -49,11 +49,11 @@ def test_fused_training_bytes_per_row():
     assert bench.train_bytes_per_row(128, 4, 128, 16, "relu") == fused(128, 4, 128, 16) + 128 == 2816
     # widths up to 64: relu' from the activations, no masks
     assert bench.train_bytes_per_row(16, 4, 16, 16, "relu", fused=True) == fused(16, 4, 16, 16) == 448
-    assert bench.train_bytes_per_row(64, 2, 64, 3, "relu") == fused(64, 2, 64, 3)
-    assert bench.train_bytes_per_row(64, 2, 64, 3, "sigmoid") == fused(64, 2, 64, 3)
+    assert bench.train_bytes_per_row(64, 2, 64, 3, "relu", fused=True) == fused(64, 2, 64, 3)
+    assert bench.train_bytes_per_row(64, 2, 64, 3, "sigmoid", fused=True) == fused(64, 2, 64, 3)
     # sine: the cos stash written and read again
     hid = 4 * 64 * 2
-    assert bench.train_bytes_per_row(64, 4, 3, 1, "sine") == fused(64, 4, 3, 1) + 2 * hid
+    assert bench.train_bytes_per_row(64, 4, 3, 1, "sine", fused=True) == fused(64, 4, 3, 1) + 2 * hid
     # outside the fused kernel's nets: the three-kernel count
     for args in [(128, 4, 128, 128, "relu"), (128, 16, 128, 128, "relu"), (128, 4, 128, 16, "sine"),
                  (64, 5, 64, 16, "sigmoid"), (64, 0, 64, 16, "relu")]:
@@ -65,11 +65,11 @@ def test_fused_training_bytes_per_row():
 
 
 def test_one_kernel_training_bytes_per_row():
-    """Widths 16 and 32 with 2 to 5 matrices run the whole step in one
+    """Widths 16, 32 and 64 with 2 to 5 matrices run the whole step in one
     kernel: X read (2 in) and T read (4 out) per row, nothing else."""
-    for w, d in [(16, 1), (16, 4), (32, 2), (32, 4)]:
+    for w, d in [(16, 1), (16, 4), (32, 2), (32, 4), (64, 1), (64, 4)]:
         assert bench.fused_step(w, d)
         assert bench.train_bytes_per_row(w, d, w, 16, "relu") == 2 * w + 64
         assert bench.train_bytes_per_row(w, d, 7, 3, "sine") == 14 + 12
-    for w, d in [(16, 0), (16, 5), (32, 16), (64, 4), (128, 4)]:
+    for w, d in [(16, 0), (16, 5), (32, 16), (64, 0), (64, 5), (128, 4)]:
         assert not bench.fused_step(w, d)
