@@ -87,6 +87,27 @@ __device__ __forceinline__ float act_out_grad(int act, float c, float y) {
   }
 }
 
+// The training epilogue of one 16-row block of an output strip, OA the
+// output activation: acc holds the pre-activations C (lane (g, i): row i,
+// columns j0 .. j0 + 3), t the targets, `valid` which of the four are real
+// (row < M, column < out_dim).  Returns Y as two packed bf16 pairs in y and
+// the output delta scale (Y - T) sigma_out'(C) in d (0 where not valid), and
+// adds (Y - T)^2 of the valid ones to loss.  Y and the loss use the fp32 Y.
+template <int OA>
+__device__ __forceinline__ void train_epilogue(const f32x4& acc, const u32x4& t, const bool (&valid)[4],
+                                               float scale, float& loss, u32x2& y, u32x2& d) {
+  float yv[4], dv[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) {
+    yv[q] = act_apply(OA, acc[q]);
+    const float diff = yv[q] - __uint_as_float(t[q]);
+    if (valid[q]) loss += diff * diff;
+    dv[q] = valid[q] ? (scale * diff) * act_out_grad(OA, acc[q], yv[q]) : 0.f;
+  }
+  y = u32x2{pack_bf16x2(yv[0], yv[1]), pack_bf16x2(yv[2], yv[3])};
+  d = u32x2{pack_bf16x2(dv[0], dv[1]), pack_bf16x2(dv[2], dv[3])};
+}
+
 // Derivative of a hidden activation from what the forward pass stored: the
 // bf16 activation a (ReLU: a > 0, sigmoid: a (1 - a)) or, for sine, the
 // stored bf16 cos(c) passed in as a.
@@ -141,6 +162,10 @@ constexpr int kStoreNT = 2;  // the nt bit of the buffer instructions' cache pol
 template <bool NT = true>
 __device__ __forceinline__ void bstore32(uint32_t v, rsrc_t r, uint32_t voff, uint32_t soff) {
   __builtin_amdgcn_raw_buffer_store_b32(v, r, voff, soff, NT ? kStoreNT : 0);
+}
+template <bool NT = true>
+__device__ __forceinline__ void bstore16(uint32_t v, rsrc_t r, uint32_t voff, uint32_t soff) {
+  __builtin_amdgcn_raw_buffer_store_b16((unsigned short)v, r, voff, soff, NT ? kStoreNT : 0);
 }
 template <bool NT = true>
 __device__ __forceinline__ void bstore64(u32x2 v, rsrc_t r, uint32_t voff, uint32_t soff) {

@@ -59,7 +59,7 @@ struct TrainfGeom {
                 "fused training step: widths 16 and 32, 2 .. kTrainfMaxL matrices");
 };
 
-template <int W, int L, int OS, int ACT>
+template <int W, int L, int OS, int ACT, bool VEC>
 __global__ __launch_bounds__(kTrainfWaves * 64) void trainf_kernel(const TrainfArgs a) {
   using Gm = TrainfGeom<W, L, OS>;
   constexpr int NW = Gm::NW, NT = Gm::NT, SW = Gm::SW, KBW = Gm::KBW;
@@ -72,8 +72,8 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainf_kernel(const TrainfA
   const int64_t M = a.M;
   const int in_dim = a.in_dim, out_dim = a.out_dim, out_act = a.out_act;
   const int SO = (out_dim + 15) >> 4;
-  const bool xvec = (in_dim & 7) == 0;
-  const bool yvec = (out_dim & 3) == 0;
+  const bool xvec = VEC || (in_dim & 7) == 0;
+  const bool yvec = VEC || (out_dim & 3) == 0;
 
   // Resident weights, both orientations (direct-to-LDS loads).
   stage_frags(smem, a.packedF, a.fwd_total, wave, NW, lane);
@@ -132,18 +132,19 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainf_kernel(const TrainfA
         for (int n = 0; n < NT; ++n) xin[n][kb] = bload128(xr, voff, (uint32_t)(n * 32 * in_dim));
       }
     } else {
+      // other input widths: one 2-byte load per feature (0 past in_dim or M)
+      const rsrc_t xr = make_rsrc(a.X + r.row0 * in_dim, r.vr * in_dim * 2);
 #pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        const int64_t m = r.row0 + n * 16 + li;
+      for (int kb = 0; kb < KBW; ++kb) {
+        const int f0 = kb * 32 + lg * 8;
+        uint32_t vo[8];
 #pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) {
-          const int f0 = kb * 32 + lg * 8;
-          uint32_t e[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
-          if (m < M && f0 < in_dim) {
-            const uint16_t* xp = a.X + m * in_dim + f0;
+        for (int q = 0; q < 8; ++q) vo[q] = f0 + q < in_dim ? (uint32_t)((li * in_dim + f0 + q) * 2) : kOOB;
 #pragma unroll
-            for (int q = 0; q < 8; ++q) e[q] = (f0 + q < in_dim) ? (uint32_t)xp[q] : 0u;
-          }
+        for (int n = 0; n < NT; ++n) {
+          uint32_t e[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q) e[q] = bload16(xr, vo[q], (uint32_t)(n * 32 * in_dim));
           xin[n][kb] = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
                              e[6] | (e[7] << 16)};
         }
@@ -153,21 +154,19 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainf_kernel(const TrainfA
 #pragma unroll
     for (int s = 0; s < OS; ++s) {
       const int j0 = s * 16 + lg * 4;
+      if (yvec) {
+        const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
 #pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        if (yvec) {
-          const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
-          tq[n][s] = bload128(tr, eo * 4, (uint32_t)(n * 64 * out_dim));
-        } else {
-          const int64_t m = r.row0 + n * 16 + li;
-          uint32_t t[4] = {0u, 0u, 0u, 0u};
-          if (m < M && j0 < out_dim) {
-            const float* tp = a.T + m * out_dim + j0;
+        for (int n = 0; n < NT; ++n) tq[n][s] = bload128(tr, eo * 4, (uint32_t)(n * 64 * out_dim));
+      } else {
+        uint32_t vo[4];
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-              if (j0 + q < out_dim) t[q] = __float_as_uint(tp[q]);
-          }
-          tq[n][s] = u32x4{t[0], t[1], t[2], t[3]};
+        for (int q = 0; q < 4; ++q) vo[q] = j0 + q < out_dim ? (uint32_t)((li * out_dim + j0 + q) * 4) : kOOB;
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+          const uint32_t so = (uint32_t)(n * 64 * out_dim);
+          tq[n][s] = u32x4{bload32(tr, vo[0], so), bload32(tr, vo[1], so), bload32(tr, vo[2], so),
+                           bload32(tr, vo[3], so)};
         }
       }
     }
@@ -239,7 +238,9 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainf_kernel(const TrainfA
     for (int n = 0; n < NT; ++n)
 #pragma unroll
       for (int kb = 0; kb < KBW; ++kb) dA[n][kb] = u32x4{0u, 0u, 0u, 0u};
-    {
+    // One copy of the output layer per output activation, chosen once.
+    auto output_layer = [&](auto oc) {
+      constexpr int OA = decltype(oc)::value;
       const u32x4* wl = smem + (size_t)Gm::fwd_off(L - 1) * 64;
       const rsrc_t yr = make_rsrc(a.Y + r.row0 * out_dim, a.Y ? r.vr * out_dim * 2 : 0);
       static_for<0, OS>([&](auto sc) {
@@ -256,44 +257,39 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainf_kernel(const TrainfA
 #pragma unroll
           for (int kb = 0; kb < KBW; ++kb)
             acc = mfma16(af[kb], in_op(std::integral_constant<int, L - 1>{}, n, kb), acc);
-          const int64_t m = r.row0 + n * 16 + li;
-          const bool ok = (m < M) && (j0 < out_dim);
-          float y[4];
+          const bool row_ok = n * 16 + li < r.vr;
+          bool valid[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) y[q] = act_apply(out_act, acc[q]);
-          const uint32_t y0 = pack_bf16x2(y[0], y[1]), y1 = pack_bf16x2(y[2], y[3]);
+          for (int q = 0; q < 4; ++q) valid[q] = row_ok && j0 + q < out_dim;
+          u32x2 y, d;
+          train_epilogue<OA>(acc, tq[n][s], valid, a.scale, loss, y, d);
           if (a.Y != nullptr) {
+            const uint32_t so = (uint32_t)(n * 32 * out_dim);
             if (yvec) {
-              bstore64(u32x2{y0, y1}, yr, eo * 2, (uint32_t)(n * 32 * out_dim));
-            } else if (ok) {
-              uint16_t* yp = a.Y + m * out_dim + j0;
-              const uint16_t yb[4] = {(uint16_t)(y0 & 0xffff), (uint16_t)(y0 >> 16),
-                                      (uint16_t)(y1 & 0xffff), (uint16_t)(y1 >> 16)};
+              bstore64(y, yr, eo * 2, so);
+            } else {
+              // one 2-byte store per column (dropped past out_dim or M)
 #pragma unroll
               for (int q = 0; q < 4; ++q)
-                if (j0 + q < out_dim) yp[q] = yb[q];
+                bstore16(((q < 2 ? y.x : y.y) >> (16 * (q & 1))) & 0xffffu, yr,
+                         j0 + q < out_dim ? (uint32_t)((li * out_dim + j0 + q) * 2) : kOOB, so);
             }
           }
-          const float t[4] = {__uint_as_float(tq[n][s].x), __uint_as_float(tq[n][s].y),
-                              __uint_as_float(tq[n][s].z), __uint_as_float(tq[n][s].w)};
-          float d[4];
-#pragma unroll
-          for (int q = 0; q < 4; ++q) {
-            const bool valid = ok && (j0 + q < out_dim);
-            const float diff = y[q] - t[q];
-            if (valid) loss += diff * diff;
-            d[q] = valid ? (a.scale * diff) * act_out_grad(out_act, acc[q], y[q]) : 0.f;
-          }
-          const uint32_t p0 = pack_bf16x2(d[0], d[1]), p1 = pack_bf16x2(d[2], d[3]);
           if constexpr (s & 1) {
-            dA[n][s >> 1].z = p0;
-            dA[n][s >> 1].w = p1;
+            dA[n][s >> 1].z = d.x;
+            dA[n][s >> 1].w = d.y;
           } else {
-            dA[n][s >> 1].x = p0;
-            dA[n][s >> 1].y = p1;
+            dA[n][s >> 1].x = d.x;
+            dA[n][s >> 1].y = d.y;
           }
         }
       });
+    };
+    switch (out_act) {
+      case ACT_RELU: output_layer(std::integral_constant<int, ACT_RELU>{}); break;
+      case ACT_SIGMOID: output_layer(std::integral_constant<int, ACT_SIGMOID>{}); break;
+      case ACT_SINE: output_layer(std::integral_constant<int, ACT_SINE>{}); break;
+      default: output_layer(std::integral_constant<int, ACT_LINEAR>{}); break;
     }
 
     // ---- backward.  X again, as strips, for G_0 (from cache: the wave
@@ -305,7 +301,7 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainf_kernel(const TrainfA
 #pragma unroll
       for (int s = 0; s < SW; ++s) {
         const int f0 = 16 * s + 4 * lg;
-        if ((in_dim & 3) == 0) {
+        if (VEC || (in_dim & 3) == 0) {
           const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
 #pragma unroll
           for (int n = 0; n < NT; ++n) xs[n][s] = bload64(xr, voff, (uint32_t)(n * 32 * in_dim));
@@ -454,7 +450,7 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainf_kernel(const TrainfA
   }
 }
 
-template <int W, int L, int OS, int ACT>
+template <int W, int L, int OS, int ACT, bool VEC>
 static hipError_t trainf_launch_t(const TrainfArgs& a0, hipStream_t stream, int* grid_out) {
   using Gm = TrainfGeom<W, L, OS>;
   TrainfArgs a = a0;
@@ -465,7 +461,7 @@ static hipError_t trainf_launch_t(const TrainfArgs& a0, hipStream_t stream, int*
   if (e != hipSuccess) return e;
   const size_t lds = Gm::lds_bytes();
   if (lds > (size_t)di.max_lds) return hipErrorNotSupported;
-  auto kern = trainf_kernel<W, L, OS, ACT>;
+  auto kern = trainf_kernel<W, L, OS, ACT, VEC>;
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), kTrainfWaves * 64, lds, &occ);
   if (e != hipSuccess) return e;
@@ -478,24 +474,34 @@ static hipError_t trainf_launch_t(const TrainfArgs& a0, hipStream_t stream, int*
   return hipGetLastError();
 }
 
-template <int W, int OS, int ACT>
+template <int W, int OS, int ACT, bool VEC>
 static hipError_t trainf_by_l(int L, const TrainfArgs& a, hipStream_t s, int* g) {
   switch (L) {
-    case 2: return trainf_launch_t<W, 2, OS, ACT>(a, s, g);
-    case 3: return trainf_launch_t<W, 3, OS, ACT>(a, s, g);
-    case 4: return trainf_launch_t<W, 4, OS, ACT>(a, s, g);
-    case 5: return trainf_launch_t<W, 5, OS, ACT>(a, s, g);
+    case 2: return trainf_launch_t<W, 2, OS, ACT, VEC>(a, s, g);
+    case 3: return trainf_launch_t<W, 3, OS, ACT, VEC>(a, s, g);
+    case 4: return trainf_launch_t<W, 4, OS, ACT, VEC>(a, s, g);
+    case 5: return trainf_launch_t<W, 5, OS, ACT, VEC>(a, s, g);
     default: return hipErrorNotSupported;
   }
+}
+
+// VEC: X rows a multiple of 8 features and Y rows of 4 (16- and 8-byte
+// accesses only), the common case, compiled without the per-element paths:
+// measured at 2^20 rows with the output activation also fixed, width 16
+// 38.2 -> 32.5 us, width 32 63.3 -> 52.2 us, width 64 201.9 -> 182.7 us.
+template <int W, int OS, int ACT>
+static hipError_t trainf_by_vec(int L, const TrainfArgs& a, hipStream_t s, int* g) {
+  if (a.in_dim % 8 == 0 && a.out_dim % 4 == 0) return trainf_by_l<W, OS, ACT, true>(L, a, s, g);
+  return trainf_by_l<W, OS, ACT, false>(L, a, s, g);
 }
 
 template <int W, int OS>
 static hipError_t trainf_by_act(int act, int L, const TrainfArgs& a, hipStream_t s, int* g) {
   switch (act) {
-    case ACT_RELU: return trainf_by_l<W, OS, ACT_RELU>(L, a, s, g);
-    case ACT_SIGMOID: return trainf_by_l<W, OS, ACT_SIGMOID>(L, a, s, g);
-    case ACT_SINE: return trainf_by_l<W, OS, ACT_SINE>(L, a, s, g);
-    default: return trainf_by_l<W, OS, ACT_LINEAR>(L, a, s, g);
+    case ACT_RELU: return trainf_by_vec<W, OS, ACT_RELU>(L, a, s, g);
+    case ACT_SIGMOID: return trainf_by_vec<W, OS, ACT_SIGMOID>(L, a, s, g);
+    case ACT_SINE: return trainf_by_vec<W, OS, ACT_SINE>(L, a, s, g);
+    default: return trainf_by_vec<W, OS, ACT_LINEAR>(L, a, s, g);
   }
 }
 

@@ -54,7 +54,7 @@ struct TrainwGeom {
   static_assert(L >= 2 && L <= kTrainfMaxL && (OS == 1 || OS == 4), "width-64 fused training step");
 };
 
-template <int L, int OS, int ACT>
+template <int L, int OS, int ACT, bool VEC>
 __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfArgs a) {
   using Gm = TrainwGeom<L, OS>;
   constexpr int NW = Gm::NW, SW = Gm::SW, KBW = Gm::KBW, KBO = Gm::KBO, LDT = Gm::LDT, KS = Gm::KS;
@@ -70,8 +70,8 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
   const int in_dim = a.in_dim, out_dim = a.out_dim, out_act = a.out_act;
   const int SO = (out_dim + 15) >> 4;
   const int SI = (in_dim + 15) >> 4;  // strips of X
-  const bool xvec = (in_dim & 7) == 0;
-  const bool yvec = (out_dim & 3) == 0;
+  const bool xvec = VEC || (in_dim & 7) == 0;
+  const bool yvec = VEC || (out_dim & 3) == 0;
 
   // Resident weights (direct-to-LDS loads, waited for below).
   stage_frags(smem, a.packedF, a.fwd_total, wave, NW, lane);
@@ -164,16 +164,15 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
         xin[kb] = bload128(xr, voff, 0u);
       }
     } else {
-      const int64_t m = r.row0 + li;
+      // other input widths: one 2-byte load per feature (0 past in_dim or M)
+      const rsrc_t xr = make_rsrc(a.X + r.row0 * in_dim, r.vr * in_dim * 2);
 #pragma unroll
       for (int kb = 0; kb < KBW; ++kb) {
         const int f0 = kb * 32 + lg * 8;
-        uint32_t e[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
-        if (m < M && f0 < in_dim) {
-          const uint16_t* xp = a.X + m * in_dim + f0;
+        uint32_t e[8];
 #pragma unroll
-          for (int q = 0; q < 8; ++q) e[q] = (f0 + q < in_dim) ? (uint32_t)xp[q] : 0u;
-        }
+        for (int q = 0; q < 8; ++q)
+          e[q] = bload16(xr, f0 + q < in_dim ? (uint32_t)((li * in_dim + f0 + q) * 2) : kOOB, 0u);
         xin[kb] = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
                         e[6] | (e[7] << 16)};
       }
@@ -186,14 +185,10 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
         const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
         tq[s] = bload128(tr, eo * 4, 0u);
       } else {
-        const int64_t m = r.row0 + li;
-        uint32_t t[4] = {0u, 0u, 0u, 0u};
-        if (m < M && j0 < out_dim) {
-          const float* tp = a.T + m * out_dim + j0;
+        uint32_t t[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            if (j0 + q < out_dim) t[q] = __float_as_uint(tp[q]);
-        }
+        for (int q = 0; q < 4; ++q)
+          t[q] = bload32(tr, j0 + q < out_dim ? (uint32_t)((li * out_dim + j0 + q) * 4) : kOOB, 0u);
         tq[s] = u32x4{t[0], t[1], t[2], t[3]};
       }
     }
@@ -265,10 +260,12 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
     u32x4 dA[KBW], dB[KBW];
 #pragma unroll
     for (int kb = 0; kb < KBW; ++kb) dA[kb] = u32x4{0u, 0u, 0u, 0u};
-    {
+    // One copy of the output layer per output activation, chosen once.
+    auto output_layer = [&](auto oc) {
+      constexpr int OA = decltype(oc)::value;
       const u32x4* wl = smem + (size_t)Gm::fwd_off(L - 1) * 64;
       const rsrc_t yr = make_rsrc(a.Y + r.row0 * out_dim, a.Y ? r.vr * out_dim * 2 : 0);
-      const int64_t m = r.row0 + li;
+      const bool row_ok = li < r.vr;
       static_for<0, OS>([&](auto sc) {
         constexpr int s = decltype(sc)::value;
         if (s >= SO) return;
@@ -279,43 +276,36 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) acc = mfma16(af[kb], ach[L - 2][kb], acc);
         const int j0 = s * 16 + lg * 4;
-        const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
-        const bool ok = (m < M) && (j0 < out_dim);
-        float y[4];
+        bool valid[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) y[q] = act_apply(out_act, acc[q]);
-        const uint32_t y0 = pack_bf16x2(y[0], y[1]), y1 = pack_bf16x2(y[2], y[3]);
+        for (int q = 0; q < 4; ++q) valid[q] = row_ok && j0 + q < out_dim;
+        u32x2 y, d;
+        train_epilogue<OA>(acc, tq[s], valid, a.scale, loss, y, d);
         if (a.Y != nullptr) {
           if (yvec) {
-            bstore64(u32x2{y0, y1}, yr, eo * 2, 0u);
-          } else if (ok) {
-            uint16_t* yp = a.Y + m * out_dim + j0;
-            const uint16_t yb[4] = {(uint16_t)(y0 & 0xffff), (uint16_t)(y0 >> 16),
-                                    (uint16_t)(y1 & 0xffff), (uint16_t)(y1 >> 16)};
+            bstore64(y, yr, (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) * 2 : kOOB, 0u);
+          } else {
+            // one 2-byte store per column (dropped past out_dim or M)
 #pragma unroll
             for (int q = 0; q < 4; ++q)
-              if (j0 + q < out_dim) yp[q] = yb[q];
+              bstore16(((q < 2 ? y.x : y.y) >> (16 * (q & 1))) & 0xffffu, yr,
+                       j0 + q < out_dim ? (uint32_t)((li * out_dim + j0 + q) * 2) : kOOB, 0u);
           }
         }
-        const float t[4] = {__uint_as_float(tq[s].x), __uint_as_float(tq[s].y),
-                            __uint_as_float(tq[s].z), __uint_as_float(tq[s].w)};
-        float d[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-          const bool valid = ok && (j0 + q < out_dim);
-          const float diff = y[q] - t[q];
-          if (valid) loss += diff * diff;
-          d[q] = valid ? (a.scale * diff) * act_out_grad(out_act, acc[q], y[q]) : 0.f;
-        }
-        const uint32_t p0 = pack_bf16x2(d[0], d[1]), p1 = pack_bf16x2(d[2], d[3]);
         if constexpr (s & 1) {
-          dA[s >> 1].z = p0;
-          dA[s >> 1].w = p1;
+          dA[s >> 1].z = d.x;
+          dA[s >> 1].w = d.y;
         } else {
-          dA[s >> 1].x = p0;
-          dA[s >> 1].y = p1;
+          dA[s >> 1].x = d.x;
+          dA[s >> 1].y = d.y;
         }
       });
+    };
+    switch (out_act) {
+      case ACT_RELU: output_layer(std::integral_constant<int, ACT_RELU>{}); break;
+      case ACT_SIGMOID: output_layer(std::integral_constant<int, ACT_SIGMOID>{}); break;
+      case ACT_SINE: output_layer(std::integral_constant<int, ACT_SINE>{}); break;
+      default: output_layer(std::integral_constant<int, ACT_LINEAR>{}); break;
     }
 
     // ---- backward.  X of the wave's rows once more, in chain order (the
@@ -329,7 +319,7 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
 #pragma unroll
       for (int s = 0; s < SW; ++s) {
         const int f0 = 16 * s + 4 * lg;
-        if ((in_dim & 3) == 0) {
+        if (VEC || (in_dim & 3) == 0) {
           const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
           const u32x2 v = bload64(xr, voff, 0u);
           h[s][0] = v.x;
@@ -473,7 +463,7 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
   }
 }
 
-template <int L, int OS, int ACT>
+template <int L, int OS, int ACT, bool VEC>
 static hipError_t trainw_launch_t(const TrainfArgs& a0, hipStream_t stream, int* grid_out) {
   using Gm = TrainwGeom<L, OS>;
   TrainfArgs a = a0;
@@ -484,7 +474,7 @@ static hipError_t trainw_launch_t(const TrainfArgs& a0, hipStream_t stream, int*
   if (e != hipSuccess) return e;
   const size_t lds = Gm::lds_bytes();
   if (lds > (size_t)di.max_lds) return hipErrorNotSupported;
-  auto kern = trainw_kernel<L, OS, ACT>;
+  auto kern = trainw_kernel<L, OS, ACT, VEC>;
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), kTrainfWaves * 64, lds, &occ);
   if (e != hipSuccess) return e;
@@ -497,24 +487,31 @@ static hipError_t trainw_launch_t(const TrainfArgs& a0, hipStream_t stream, int*
   return hipGetLastError();
 }
 
-template <int OS, int ACT>
+template <int OS, int ACT, bool VEC>
 static hipError_t trainw_by_l(int L, const TrainfArgs& a, hipStream_t s, int* g) {
   switch (L) {
-    case 2: return trainw_launch_t<2, OS, ACT>(a, s, g);
-    case 3: return trainw_launch_t<3, OS, ACT>(a, s, g);
-    case 4: return trainw_launch_t<4, OS, ACT>(a, s, g);
-    case 5: return trainw_launch_t<5, OS, ACT>(a, s, g);
+    case 2: return trainw_launch_t<2, OS, ACT, VEC>(a, s, g);
+    case 3: return trainw_launch_t<3, OS, ACT, VEC>(a, s, g);
+    case 4: return trainw_launch_t<4, OS, ACT, VEC>(a, s, g);
+    case 5: return trainw_launch_t<5, OS, ACT, VEC>(a, s, g);
     default: return hipErrorNotSupported;
   }
+}
+
+// VEC: X rows a multiple of 8 features and Y rows of 4 (see trainf_by_vec).
+template <int OS, int ACT>
+static hipError_t trainw_by_vec(int L, const TrainfArgs& a, hipStream_t s, int* g) {
+  if (a.in_dim % 8 == 0 && a.out_dim % 4 == 0) return trainw_by_l<OS, ACT, true>(L, a, s, g);
+  return trainw_by_l<OS, ACT, false>(L, a, s, g);
 }
 
 template <int OS>
 static hipError_t trainw_by_act(int act, int L, const TrainfArgs& a, hipStream_t s, int* g) {
   switch (act) {
-    case ACT_RELU: return trainw_by_l<OS, ACT_RELU>(L, a, s, g);
-    case ACT_SIGMOID: return trainw_by_l<OS, ACT_SIGMOID>(L, a, s, g);
-    case ACT_SINE: return trainw_by_l<OS, ACT_SINE>(L, a, s, g);
-    default: return trainw_by_l<OS, ACT_LINEAR>(L, a, s, g);
+    case ACT_RELU: return trainw_by_vec<OS, ACT_RELU>(L, a, s, g);
+    case ACT_SIGMOID: return trainw_by_vec<OS, ACT_SIGMOID>(L, a, s, g);
+    case ACT_SINE: return trainw_by_vec<OS, ACT_SINE>(L, a, s, g);
+    default: return trainw_by_vec<OS, ACT_LINEAR>(L, a, s, g);
   }
 }
 
