@@ -77,7 +77,7 @@ constexpr int fwd_nt() {
   return TileCfg<W>::NT;
 }
 
-template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false>
+template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false, bool LIN = false>
 __global__ __launch_bounds__((fwd_waves<W, MODE, SMALL, FU>() * 64)) void fwd_kernel(const FwdArgs a) {
   constexpr int NT = fwd_nt<W, MODE, SMALL, FU>(), NW = fwd_waves<W, MODE, SMALL, FU>();
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
@@ -92,7 +92,7 @@ __global__ __launch_bounds__((fwd_waves<W, MODE, SMALL, FU>() * 64)) void fwd_ke
   const int OP = SO * 16;
   const bool xvec = (in_dim & 7) == 0;
   const bool yvec = (out_dim & 3) == 0;
-  const int out_act = a.out_act;
+  const int out_act = LIN ? (int)ACT_LINEAR : a.out_act;
   constexpr bool resident = RES;
   // Non-temporal stores, except for inference with streamed weights: there
   // every layer ends by waiting for all outstanding memory operations, the
@@ -544,13 +544,17 @@ struct FwdPick {
   int threads;
   int64_t rows;
 };
-template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false>
+template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false, bool LIN = false>
 static FwdPick fwd_pick() {
   constexpr int NW = fwd_waves<W, MODE, SMALL, FU>(), NT = fwd_nt<W, MODE, SMALL, FU>();
-  return FwdPick{fwd_kernel<W, ACT, MODE, FU, RES, SMALL>, NW * 64, (int64_t)NW * NT * 16};
+  return FwdPick{fwd_kernel<W, ACT, MODE, FU, RES, SMALL, LIN>, NW * 64, (int64_t)NW * NT * 16};
 }
 
-template <int W, int ACT, int MODE>
+// LIN: the output activation is linear (the common case) and fixed at
+// compile time.  With a runtime output activation the epilogue switches per
+// element, which cost 12% of width-16 inference at 2^20 rows (17.9 -> 15.7
+// us) and 1-2% at the other widths.
+template <int W, int ACT, int MODE, bool LIN>
 static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out) {
   FwdArgs a = a0;
   DeviceInfo di;
@@ -566,13 +570,15 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
   // (1297 against 1334 us for the whole step), so it keeps 1 KiB spare.
   a.resident = res_bytes + (MODE == FWD_INFER ? 0 : 1024) <= (size_t)di.max_lds ? 1 : 0;
   const size_t lds = a.resident ? res_bytes : (size_t)2 * maxf * 1024;
-  FwdPick pk = a.resident ? fwd_pick<W, ACT, MODE, 0, true>() : fwd_pick<W, ACT, MODE, 0, false>();
+  FwdPick pk = a.resident ? fwd_pick<W, ACT, MODE, 0, true, false, LIN>() : fwd_pick<W, ACT, MODE, 0, false, false, LIN>();
   if constexpr (MODE == FWD_INFER && W >= 64) {
     if (a.resident && a.L >= 2 && SO == 1 && (a.in_dim % 8) == 0)
-      pk = (a.L & 1) ? fwd_pick<W, ACT, MODE, 1, true>() : fwd_pick<W, ACT, MODE, 2, true>();
+      pk = (a.L & 1) ? fwd_pick<W, ACT, MODE, 1, true, false, LIN>() : fwd_pick<W, ACT, MODE, 2, true, false, LIN>();
     else if (a.L >= 2 && (a.in_dim % 8) == 0)
-      pk = a.resident ? ((a.L & 1) ? fwd_pick<W, ACT, MODE, 4, true>() : fwd_pick<W, ACT, MODE, 3, true>())
-                      : ((a.L & 1) ? fwd_pick<W, ACT, MODE, 4, false>() : fwd_pick<W, ACT, MODE, 3, false>());
+      pk = a.resident ? ((a.L & 1) ? fwd_pick<W, ACT, MODE, 4, true, false, LIN>()
+                                   : fwd_pick<W, ACT, MODE, 3, true, false, LIN>())
+                      : ((a.L & 1) ? fwd_pick<W, ACT, MODE, 4, false, false, LIN>()
+                                   : fwd_pick<W, ACT, MODE, 3, false, false, LIN>());
   }
   if constexpr (W <= 64) {
     // Small batches: fewer than two row tiles of the tile configuration
@@ -580,7 +586,7 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
     // several workgroups per CU), inference and training forward alike.
     const int64_t cfg_rows = (int64_t)TileCfg<W>::NT * TileCfg<W>::NW * 16;
     if ((a.M + cfg_rows - 1) / cfg_rows <= 2 * (int64_t)di.cus && a.resident)
-      pk = fwd_pick<W, ACT, MODE, 0, true, true>();
+      pk = fwd_pick<W, ACT, MODE, 0, true, true, LIN>();
   }
   a.ntiles = (int)((a.M + pk.rows - 1) / pk.rows);
   int occ = 0;
@@ -598,9 +604,13 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
 template <int W, int ACT>
 static hipError_t by_mode(int mode, const FwdArgs& a, hipStream_t s, int* g) {
   switch (mode) {
-    case FWD_INFER: return launch_t<W, ACT, FWD_INFER>(a, s, g);
-    case FWD_STASH: return launch_t<W, ACT, FWD_STASH>(a, s, g);
-    default: return launch_t<W, ACT, FWD_TRAIN>(a, s, g);
+    case FWD_INFER:
+      return a.out_act == ACT_LINEAR ? launch_t<W, ACT, FWD_INFER, true>(a, s, g)
+                                     : launch_t<W, ACT, FWD_INFER, false>(a, s, g);
+    case FWD_STASH: return launch_t<W, ACT, FWD_STASH, false>(a, s, g);
+    default:
+      return a.out_act == ACT_LINEAR ? launch_t<W, ACT, FWD_TRAIN, true>(a, s, g)
+                                     : launch_t<W, ACT, FWD_TRAIN, false>(a, s, g);
   }
 }
 
