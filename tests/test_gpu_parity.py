@@ -559,6 +559,24 @@ def test_fused_backward_shapes(ffmlp, gpu, width, depth, in_dim, out_dim, act, o
     log("  seeded grad errs", ["%.2e" % e for e in errs])
 
 
+@pytest.mark.parametrize("width,depth,in_dim,out_dim,act,out_act,M", [
+    (16, 1, 5, 3, "sine", "sigmoid", 1), (16, 4, 16, 16, "relu", "linear", 257),
+    (16, 3, 12, 7, "sigmoid", "relu", 4099),
+    (32, 2, 31, 32, "sigmoid", "relu", 513), (32, 3, 8, 4, "linear", "sine", 1025),
+    (32, 4, 32, 20, "sine", "linear", 9000),
+    (64, 1, 1, 1, "relu", "linear", 129), (64, 4, 64, 64, "sine", "linear", 3000),
+    (64, 3, 12, 17, "sigmoid", "sigmoid", 700), (64, 2, 40, 16, "linear", "relu", 65541),
+])
+def test_one_kernel_step_shapes(ffmlp, gpu, width, depth, in_dim, out_dim, act, out_act, M):
+    """The one-kernel training step (widths 16, 32, 64 with 2 to 5 matrices)
+    across its variants: vector and per-element X, T and Y paths (in_dim a
+    multiple of 8 or not, out_dim a multiple of 4 or not), one and several
+    output strips, every hidden and output activation, a single row, ragged
+    tiles and several tiles per workgroup.  Y (bitwise equal to inference),
+    G and the loss against the oracle."""
+    run_case(ffmlp, gpu, width, depth, in_dim, out_dim, M, act, out_act, seed=50 + width + depth)
+
+
 def test_argument_errors_on_device(ffmlp, gpu):
     net = ffmlp.FusedMLP(64, 2, 64, 16, "relu")
     W, X, T = inputs(15, 64, 2, 64, 16, 100)
