@@ -8,10 +8,12 @@
 // backward kernel: wave w keeps fixed slices of every G_i in registers over
 // all of its workgroup's tiles.  What that kernel reads from the stash in
 // HBM, this one computes itself: a workgroup of eight waves owns a tile of
-// 128 rows, each wave takes its 16 rows through the forward layers (the
-// forward kernel's arithmetic, so Y is bitwise the inference Y) and keeps
-// every hidden activation (and for sine the bf16 cos of the pre-activation)
-// in VGPRs.  Per backward layer each wave writes its rows' D_{i+1} and A_i,
+// 8 NT 16-row blocks, each wave takes its NT blocks through the forward
+// layers (the forward kernel's arithmetic, so Y is bitwise the inference Y)
+// and keeps every hidden activation (and for sine the bf16 cos of the
+// pre-activation) in VGPRs.  NT is 2 (256-row tiles: every weight fragment
+// read from LDS feeds two MFMAs) except for sine nets, whose cos source
+// leaves registers for one block only.  Per backward layer each wave writes its rows' D_{i+1} and A_i,
 // transposed on the matrix cores (MFMA against 0/1 selection matrices), into
 // two LDS tiles DT and AT [feature][row]; after a barrier every wave
 // accumulates its G slices from them over the tile's 128 rows, interleaved
@@ -23,12 +25,12 @@
 
 namespace ffmlp {
 
-template <int L, int OS>
+template <int L, int OS, int NT>
 struct TrainwGeom {
   static constexpr int W = 64, NW = kTrainfWaves, SW = 4, KBW = 2;
   static constexpr int KBO = (OS * 16 + 31) / 32;  // k-blocks of the output delta
-  static constexpr int ROWS = NW * 16;             // rows per tile, 16 per wave
-  static constexpr int LDT = ROWS;                 // DT / AT row: 128 rows of bf16
+  static constexpr int ROWS = NW * NT * 16;        // rows per tile
+  static constexpr int LDT = ROWS;                 // DT / AT row: the tile's rows in bf16
   static constexpr int KS = ROWS / 32;             // 32-row contraction steps per tile
   // LDS: forward layers 0 .. L-1 (the output layer's OS strips at most),
   // backward layers 1 .. L-2 whole and the output layer's first KBO
@@ -51,12 +53,24 @@ struct TrainwGeom {
     return o;
   }
   static constexpr int nacc() { return goff(L); }
-  static_assert(L >= 2 && L <= kTrainfMaxL && (OS == 1 || OS == 4), "width-64 fused training step");
+  static_assert(L >= 2 && L <= kTrainfMaxL && (OS == 1 || OS == 4) && (NT == 1 || NT == 2),
+                "width-64 fused training step");
 };
+
+// Two blocks per wave where the registers allow it without spilling: one
+// output strip, no cos source, and at most 4 matrices (3 when X or Y need
+// the per-element paths).  Measured at 2^20 rows: image-like net (in 32, 2
+// hidden layers, sigmoid out 3) 110 -> 95 us; the 5-matrix net spilled 12
+// VGPRs with two blocks and was slower (192 -> 202 us), so it keeps one.
+template <int L, int OS, int ACT, bool VEC>
+constexpr int trainw_nt() {
+  return (ACT != ACT_SINE && OS == 1 && L <= (VEC ? 4 : 3)) ? 2 : 1;
+}
 
 template <int L, int OS, int ACT, bool VEC>
 __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfArgs a) {
-  using Gm = TrainwGeom<L, OS>;
+  constexpr int NT = trainw_nt<L, OS, ACT, VEC>();
+  using Gm = TrainwGeom<L, OS, NT>;
   constexpr int NW = Gm::NW, SW = Gm::SW, KBW = Gm::KBW, KBO = Gm::KBO, LDT = Gm::LDT, KS = Gm::KS;
   constexpr int NACC = Gm::nacc();
   constexpr int CSL = ACT == ACT_SINE ? L - 1 : 1;  // layers of the cos source
@@ -128,13 +142,15 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
   // in DT or AT; chunk c is stored at c ^ (f % 16), which keeps the 16-byte
   // reads and the 8-byte writes free of bank conflicts.
   auto dt_off = [&](int f, int c) { return f * LDT + ((c ^ (f & 15)) << 3); };
-  // Rows 4 g .. 4 g + 3 of this wave's block, one feature per lane, go to
-  // chunk 4 (wave / 2) + g, half (wave % 2) ^ (g % 2): the order in which the
-  // 16-byte reads below hand 8 rows to an MFMA operand, the same in both
-  // tiles, so both operands pair the same rows.
-  auto put_t = [&](uint16_t* tile, int f, const f32x4& o) {
+  // Rows 4 g .. 4 g + 3 of the tile's block b (block n of wave w is
+  // b = w NT + n), one feature per lane, go to chunk 4 (b / 2) + g, half
+  // (b % 2) ^ (g % 2): the order in which the 16-byte reads below hand 8
+  // rows to an MFMA operand, the same in both tiles, so both operands pair
+  // the same rows.
+  auto put_t = [&](uint16_t* tile, int f, int n, const f32x4& o) {
+    const int b = wave * NT + n;
     const u32x2 v = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
-    *reinterpret_cast<u32x2*>(tile + dt_off(f, 4 * (wave >> 1) + lg) + 4 * ((wave & 1) ^ (lg & 1))) = v;
+    *reinterpret_cast<u32x2*>(tile + dt_off(f, 4 * (b >> 1) + lg) + 4 * ((b & 1) ^ (lg & 1))) = v;
   };
 
   drain_and_sync();  // weights in LDS
@@ -144,15 +160,15 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
   };
   auto rows_of = [&](int tile) {
     Rows r;
-    r.row0 = (int64_t)tile * Gm::ROWS + wave * 16;
+    r.row0 = (int64_t)tile * Gm::ROWS + wave * NT * 16;
     int64_t v = M - r.row0;
-    r.vr = v < 0 ? 0 : (v > 16 ? 16 : v);
+    r.vr = v < 0 ? 0 : (v > NT * 16 ? NT * 16 : v);
     return r;
   };
-  // X of the wave's 16 rows in input order (lane group g: features
+  // X of the wave's rows in input order (lane group g of block n: features
   // 32 kb + 8 g .. + 7, the first layer's packing) and T of its output
-  // strips (lane (g, i): row i, columns 16 s + 4 g .. + 3).
-  u32x4 xin[KBW], tq[OS];
+  // strips (lane (g, i): row 16 n + i, columns 16 s + 4 g .. + 3).
+  u32x4 xin[NT][KBW], tq[NT][OS];
   auto load_xt = [&](int tile) {
     const Rows r = rows_of(tile);
     if (xvec) {
@@ -161,7 +177,8 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
       for (int kb = 0; kb < KBW; ++kb) {
         const int f0 = kb * 32 + lg * 8;
         const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
-        xin[kb] = bload128(xr, voff, 0u);
+#pragma unroll
+        for (int n = 0; n < NT; ++n) xin[n][kb] = bload128(xr, voff, (uint32_t)(n * 32 * in_dim));
       }
     } else {
       // other input widths: one 2-byte load per feature (0 past in_dim or M)
@@ -169,12 +186,16 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
 #pragma unroll
       for (int kb = 0; kb < KBW; ++kb) {
         const int f0 = kb * 32 + lg * 8;
-        uint32_t e[8];
 #pragma unroll
-        for (int q = 0; q < 8; ++q)
-          e[q] = bload16(xr, f0 + q < in_dim ? (uint32_t)((li * in_dim + f0 + q) * 2) : kOOB, 0u);
-        xin[kb] = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
-                        e[6] | (e[7] << 16)};
+        for (int n = 0; n < NT; ++n) {
+          uint32_t e[8];
+#pragma unroll
+          for (int q = 0; q < 8; ++q)
+            e[q] = bload16(xr, f0 + q < in_dim ? (uint32_t)((li * in_dim + f0 + q) * 2) : kOOB,
+                           (uint32_t)(n * 32 * in_dim));
+          xin[n][kb] = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
+                             e[6] | (e[7] << 16)};
+        }
       }
     }
     const rsrc_t tr = make_rsrc(a.T + r.row0 * out_dim, r.vr * out_dim * 4);
@@ -183,13 +204,18 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
       const int j0 = s * 16 + lg * 4;
       if (yvec) {
         const uint32_t eo = (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) : kOOB / 4;
-        tq[s] = bload128(tr, eo * 4, 0u);
-      } else {
-        uint32_t t[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q)
-          t[q] = bload32(tr, j0 + q < out_dim ? (uint32_t)((li * out_dim + j0 + q) * 4) : kOOB, 0u);
-        tq[s] = u32x4{t[0], t[1], t[2], t[3]};
+        for (int n = 0; n < NT; ++n) tq[n][s] = bload128(tr, eo * 4, (uint32_t)(n * 64 * out_dim));
+      } else {
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+          uint32_t t[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q)
+            t[q] = bload32(tr, j0 + q < out_dim ? (uint32_t)((li * out_dim + j0 + q) * 4) : kOOB,
+                           (uint32_t)(n * 64 * out_dim));
+          tq[n][s] = u32x4{t[0], t[1], t[2], t[3]};
+        }
       }
     }
   };
@@ -208,8 +234,8 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
 
     // ---- forward: a_1 .. a_{L-1} of the wave's rows in chain order (the
     // next layer's B operand; k-block kb holds strips 2 kb and 2 kb + 1).
-    u32x4 ach[L - 1][KBW];
-    u32x4 cch[CSL][KBW];  // sine: bf16 cos of the pre-activations, same order
+    u32x4 ach[L - 1][NT][KBW];
+    u32x4 cch[CSL][NT][KBW];  // sine: bf16 cos of the pre-activations, same order
     static_for<0, L - 1>([&](auto lc) {
       constexpr int l = decltype(lc)::value;
       const u32x4* wl = smem + (size_t)Gm::fwd_off(l) * 64;
@@ -218,38 +244,41 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
         u32x4 af[KBW];
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) af[kb] = wl[(s * KBW + kb) * 64 + lane];
-        f32x4 acc = zero4;
 #pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) {
-          if constexpr (l == 0) acc = mfma16(af[kb], xin[kb], acc);
-          else acc = mfma16(af[kb], ach[l - 1][kb], acc);
-        }
-        uint32_t p0, p1;
-        if constexpr (ACT == ACT_RELU) {
-          p0 = relu_bf16x2(pack_bf16x2(acc[0], acc[1]));
-          p1 = relu_bf16x2(pack_bf16x2(acc[2], acc[3]));
-        } else {
-          p0 = pack_bf16x2(act_hidden<ACT>(acc[0]), act_hidden<ACT>(acc[1]));
-          p1 = pack_bf16x2(act_hidden<ACT>(acc[2]), act_hidden<ACT>(acc[3]));
-        }
-        pin(p0);
-        pin(p1);
-        if constexpr (s & 1) {
-          ach[l][s >> 1].z = p0;
-          ach[l][s >> 1].w = p1;
-        } else {
-          ach[l][s >> 1].x = p0;
-          ach[l][s >> 1].y = p1;
-        }
-        if constexpr (ACT == ACT_SINE) {
-          const uint32_t c0 = pack_bf16x2(__cosf(acc[0]), __cosf(acc[1]));
-          const uint32_t c1 = pack_bf16x2(__cosf(acc[2]), __cosf(acc[3]));
-          if constexpr (s & 1) {
-            cch[l][s >> 1].z = c0;
-            cch[l][s >> 1].w = c1;
+        for (int n = 0; n < NT; ++n) {
+          f32x4 acc = zero4;
+#pragma unroll
+          for (int kb = 0; kb < KBW; ++kb) {
+            if constexpr (l == 0) acc = mfma16(af[kb], xin[n][kb], acc);
+            else acc = mfma16(af[kb], ach[l - 1][n][kb], acc);
+          }
+          uint32_t p0, p1;
+          if constexpr (ACT == ACT_RELU) {
+            p0 = relu_bf16x2(pack_bf16x2(acc[0], acc[1]));
+            p1 = relu_bf16x2(pack_bf16x2(acc[2], acc[3]));
           } else {
-            cch[l][s >> 1].x = c0;
-            cch[l][s >> 1].y = c1;
+            p0 = pack_bf16x2(act_hidden<ACT>(acc[0]), act_hidden<ACT>(acc[1]));
+            p1 = pack_bf16x2(act_hidden<ACT>(acc[2]), act_hidden<ACT>(acc[3]));
+          }
+          pin(p0);
+          pin(p1);
+          if constexpr (s & 1) {
+            ach[l][n][s >> 1].z = p0;
+            ach[l][n][s >> 1].w = p1;
+          } else {
+            ach[l][n][s >> 1].x = p0;
+            ach[l][n][s >> 1].y = p1;
+          }
+          if constexpr (ACT == ACT_SINE) {
+            const uint32_t c0 = pack_bf16x2(__cosf(acc[0]), __cosf(acc[1]));
+            const uint32_t c1 = pack_bf16x2(__cosf(acc[2]), __cosf(acc[3]));
+            if constexpr (s & 1) {
+              cch[l][n][s >> 1].z = c0;
+              cch[l][n][s >> 1].w = c1;
+            } else {
+              cch[l][n][s >> 1].x = c0;
+              cch[l][n][s >> 1].y = c1;
+            }
           }
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -257,47 +286,53 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
     });
 
     // ---- output layer: Y, the loss and the output delta (chain order).
-    u32x4 dA[KBW], dB[KBW];
+    u32x4 dA[NT][KBW], dB[NT][KBW];
 #pragma unroll
-    for (int kb = 0; kb < KBW; ++kb) dA[kb] = u32x4{0u, 0u, 0u, 0u};
+    for (int n = 0; n < NT; ++n)
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb) dA[n][kb] = u32x4{0u, 0u, 0u, 0u};
     // One copy of the output layer per output activation, chosen once.
     auto output_layer = [&](auto oc) {
       constexpr int OA = decltype(oc)::value;
       const u32x4* wl = smem + (size_t)Gm::fwd_off(L - 1) * 64;
       const rsrc_t yr = make_rsrc(a.Y + r.row0 * out_dim, a.Y ? r.vr * out_dim * 2 : 0);
-      const bool row_ok = li < r.vr;
       static_for<0, OS>([&](auto sc) {
         constexpr int s = decltype(sc)::value;
         if (s >= SO) return;
         u32x4 af[KBW];
 #pragma unroll
         for (int kb = 0; kb < KBW; ++kb) af[kb] = wl[(s * KBW + kb) * 64 + lane];
-        f32x4 acc = zero4;
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb) acc = mfma16(af[kb], ach[L - 2][kb], acc);
         const int j0 = s * 16 + lg * 4;
-        bool valid[4];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) valid[q] = row_ok && j0 + q < out_dim;
-        u32x2 y, d;
-        train_epilogue<OA>(acc, tq[s], valid, a.scale, loss, y, d);
-        if (a.Y != nullptr) {
-          if (yvec) {
-            bstore64(y, yr, (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) * 2 : kOOB, 0u);
-          } else {
-            // one 2-byte store per column (dropped past out_dim or M)
+        for (int n = 0; n < NT; ++n) {
+          f32x4 acc = zero4;
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
-              bstore16(((q < 2 ? y.x : y.y) >> (16 * (q & 1))) & 0xffffu, yr,
-                       j0 + q < out_dim ? (uint32_t)((li * out_dim + j0 + q) * 2) : kOOB, 0u);
+          for (int kb = 0; kb < KBW; ++kb) acc = mfma16(af[kb], ach[L - 2][n][kb], acc);
+          const bool row_ok = n * 16 + li < r.vr;
+          bool valid[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) valid[q] = row_ok && j0 + q < out_dim;
+          u32x2 y, d;
+          train_epilogue<OA>(acc, tq[n][s], valid, a.scale, loss, y, d);
+          if (a.Y != nullptr) {
+            const uint32_t so = (uint32_t)(n * 32 * out_dim);
+            if (yvec) {
+              bstore64(y, yr, (j0 < out_dim) ? (uint32_t)(li * out_dim + j0) * 2 : kOOB, so);
+            } else {
+              // one 2-byte store per column (dropped past out_dim or M)
+#pragma unroll
+              for (int q = 0; q < 4; ++q)
+                bstore16(((q < 2 ? y.x : y.y) >> (16 * (q & 1))) & 0xffffu, yr,
+                         j0 + q < out_dim ? (uint32_t)((li * out_dim + j0 + q) * 2) : kOOB, so);
+            }
           }
-        }
-        if constexpr (s & 1) {
-          dA[s >> 1].z = d.x;
-          dA[s >> 1].w = d.y;
-        } else {
-          dA[s >> 1].x = d.x;
-          dA[s >> 1].y = d.y;
+          if constexpr (s & 1) {
+            dA[n][s >> 1].z = d.x;
+            dA[n][s >> 1].w = d.y;
+          } else {
+            dA[n][s >> 1].x = d.x;
+            dA[n][s >> 1].y = d.y;
+          }
         }
       });
     };
@@ -312,53 +347,61 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
     // transposes for AT want it so; from cache: the wave read these bytes
     // at the start of the tile); then the next tile's X and T into the
     // buffers the forward no longer needs.
-    u32x4 xc[KBW];
+    u32x4 xc[NT][KBW];
     {
       const rsrc_t xr = make_rsrc(a.X + r.row0 * in_dim, r.vr * in_dim * 2);
-      uint32_t h[SW][2];
 #pragma unroll
-      for (int s = 0; s < SW; ++s) {
-        const int f0 = 16 * s + 4 * lg;
-        if (VEC || (in_dim & 3) == 0) {
-          const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
-          const u32x2 v = bload64(xr, voff, 0u);
-          h[s][0] = v.x;
-          h[s][1] = v.y;
-        } else {
-          uint32_t e[4];
+      for (int n = 0; n < NT; ++n) {
+        const uint32_t so = (uint32_t)(n * 32 * in_dim);
+        uint32_t h[SW][2];
 #pragma unroll
-          for (int q = 0; q < 4; ++q)
-            e[q] = bload16(xr, f0 + q < in_dim ? (uint32_t)((li * in_dim + f0 + q) * 2) : kOOB, 0u);
-          h[s][0] = e[0] | (e[1] << 16);
-          h[s][1] = e[2] | (e[3] << 16);
+        for (int s = 0; s < SW; ++s) {
+          const int f0 = 16 * s + 4 * lg;
+          if (VEC || (in_dim & 3) == 0) {
+            const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
+            const u32x2 v = bload64(xr, voff, so);
+            h[s][0] = v.x;
+            h[s][1] = v.y;
+          } else {
+            uint32_t e[4];
+#pragma unroll
+            for (int q = 0; q < 4; ++q)
+              e[q] = bload16(xr, f0 + q < in_dim ? (uint32_t)((li * in_dim + f0 + q) * 2) : kOOB, so);
+            h[s][0] = e[0] | (e[1] << 16);
+            h[s][1] = e[2] | (e[3] << 16);
+          }
         }
-      }
 #pragma unroll
-      for (int kb = 0; kb < KBW; ++kb) xc[kb] = u32x4{h[2 * kb][0], h[2 * kb][1], h[2 * kb + 1][0], h[2 * kb + 1][1]};
+        for (int kb = 0; kb < KBW; ++kb)
+          xc[n][kb] = u32x4{h[2 * kb][0], h[2 * kb][1], h[2 * kb + 1][0], h[2 * kb + 1][1]};
+      }
     }
     if (tile + G < a.ntiles) load_xt(tile + G);
 
     // Layer l.  Phase 1: D_{l+1} (in `cur`) and A_l (this wave's rows)
     // transposed into DT and AT.  Phase 2 (after a barrier): the wave's G_l
-    // slices over the tile's 128 rows, interleaved strip by strip with
+    // slices over the tile's rows, interleaved strip by strip with
     // D_l = (D_{l+1} W_l^T) sigma'(a_l) of its own rows into `nxt`.  A
     // barrier then frees both tiles.
-    auto layer_step = [&](auto lc, const u32x4 (&cur)[KBW], u32x4 (&nxt)[KBW]) {
+    auto layer_step = [&](auto lc, const u32x4 (&cur)[NT][KBW], u32x4 (&nxt)[NT][KBW]) {
       constexpr int l = decltype(lc)::value;
       constexpr int SD = Gm::sd(l);
-      static_for<0, SD>([&](auto sc) {
-        constexpr int s = decltype(sc)::value;
-        put_t(DT, 16 * s + li, mfma16(cur[s >> 1], (s & 1) ? sel1 : sel0, zero4));
-      });
-      static_for<0, SW>([&](auto sc) {
-        constexpr int s = decltype(sc)::value;
-        if constexpr (l == 0) {
-          if (s < SI) put_t(AT, 16 * s + li, mfma16(xc[s >> 1], (s & 1) ? sel1 : sel0, zero4));
-        } else {
-          put_t(AT, 16 * s + li, mfma16(ach[l - 1][s >> 1], (s & 1) ? sel1 : sel0, zero4));
-        }
-      });
-      __syncthreads();  // DT and AT hold the tile's 128 rows
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        static_for<0, SD>([&](auto sc) {
+          constexpr int s = decltype(sc)::value;
+          put_t(DT, 16 * s + li, n, mfma16(cur[n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+        });
+        static_for<0, SW>([&](auto sc) {
+          constexpr int s = decltype(sc)::value;
+          if constexpr (l == 0) {
+            if (s < SI) put_t(AT, 16 * s + li, n, mfma16(xc[n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+          } else {
+            put_t(AT, 16 * s + li, n, mfma16(ach[l - 1][n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+          }
+        });
+      }
+      __syncthreads();  // DT and AT hold the tile's rows
 
       int kt, jt0;
       const bool has = slice(lc, kt, jt0);
@@ -387,34 +430,37 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
           u32x4 af[KBL];
 #pragma unroll
           for (int kb = 0; kb < KBL; ++kb) af[kb] = wl[(s * KBL + kb) * 64 + lane];
-          f32x4 acc = zero4;
 #pragma unroll
-          for (int kb = 0; kb < KBL; ++kb) acc = mfma16(af[kb], cur[kb], acc);
-          // sigma'(a_l) of strip s from this wave's own activations
-          const u32x4 av = ach[l - 1][s >> 1];
-          const u32x2 v = (s & 1) ? u32x2{av.z, av.w} : u32x2{av.x, av.y};
-          uint32_t p0, p1;
-          if constexpr (ACT == ACT_RELU) {
-            p0 = mask_halves(pack_bf16x2(acc[0], acc[1]), nonzero_halves(v.x));
-            p1 = mask_halves(pack_bf16x2(acc[2], acc[3]), nonzero_halves(v.y));
-          } else if constexpr (ACT == ACT_LINEAR) {
-            p0 = pack_bf16x2(acc[0], acc[1]);
-            p1 = pack_bf16x2(acc[2], acc[3]);
-          } else {
-            u32x2 dv = v;
-            if constexpr (ACT == ACT_SINE) {
-              const u32x4 cv = cch[l - 1][s >> 1];
-              dv = (s & 1) ? u32x2{cv.z, cv.w} : u32x2{cv.x, cv.y};
+          for (int n = 0; n < NT; ++n) {
+            f32x4 acc = zero4;
+#pragma unroll
+            for (int kb = 0; kb < KBL; ++kb) acc = mfma16(af[kb], cur[n][kb], acc);
+            // sigma'(a_l) of strip s from this wave's own activations
+            const u32x4 av = ach[l - 1][n][s >> 1];
+            const u32x2 v = (s & 1) ? u32x2{av.z, av.w} : u32x2{av.x, av.y};
+            uint32_t p0, p1;
+            if constexpr (ACT == ACT_RELU) {
+              p0 = mask_halves(pack_bf16x2(acc[0], acc[1]), nonzero_halves(v.x));
+              p1 = mask_halves(pack_bf16x2(acc[2], acc[3]), nonzero_halves(v.y));
+            } else if constexpr (ACT == ACT_LINEAR) {
+              p0 = pack_bf16x2(acc[0], acc[1]);
+              p1 = pack_bf16x2(acc[2], acc[3]);
+            } else {
+              u32x2 dv = v;
+              if constexpr (ACT == ACT_SINE) {
+                const u32x4 cv = cch[l - 1][n][s >> 1];
+                dv = (s & 1) ? u32x2{cv.z, cv.w} : u32x2{cv.x, cv.y};
+              }
+              p0 = pack_bf16x2(acc[0] * der(dv.x << 16), acc[1] * der(dv.x & 0xffff0000u));
+              p1 = pack_bf16x2(acc[2] * der(dv.y << 16), acc[3] * der(dv.y & 0xffff0000u));
             }
-            p0 = pack_bf16x2(acc[0] * der(dv.x << 16), acc[1] * der(dv.x & 0xffff0000u));
-            p1 = pack_bf16x2(acc[2] * der(dv.y << 16), acc[3] * der(dv.y & 0xffff0000u));
-          }
-          if constexpr (s & 1) {
-            nxt[s >> 1].z = p0;
-            nxt[s >> 1].w = p1;
-          } else {
-            nxt[s >> 1].x = p0;
-            nxt[s >> 1].y = p1;
+            if constexpr (s & 1) {
+              nxt[n][s >> 1].z = p0;
+              nxt[n][s >> 1].w = p1;
+            } else {
+              nxt[n][s >> 1].x = p0;
+              nxt[n][s >> 1].y = p1;
+            }
           }
         }
         __builtin_amdgcn_sched_barrier(0);
@@ -465,7 +511,7 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
 
 template <int L, int OS, int ACT, bool VEC>
 static hipError_t trainw_launch_t(const TrainfArgs& a0, hipStream_t stream, int* grid_out) {
-  using Gm = TrainwGeom<L, OS>;
+  using Gm = TrainwGeom<L, OS, trainw_nt<L, OS, ACT, VEC>()>;
   TrainfArgs a = a0;
   a.ntiles = (int)((a.M + Gm::ROWS - 1) / Gm::ROWS);
   if (a.fwd_total > (uint32_t)Gm::FF) return hipErrorInvalidValue;
