@@ -57,14 +57,13 @@ struct TrainwGeom {
                 "width-64 fused training step");
 };
 
-// Two blocks per wave where the registers allow it without spilling: one
-// output strip, no cos source, and at most 4 matrices (3 when X or Y need
-// the per-element paths).  Measured at 2^20 rows: image-like net (in 32, 2
-// hidden layers, sigmoid out 3) 110 -> 95 us; the 5-matrix net spilled 12
-// VGPRs with two blocks and was slower (192 -> 202 us), so it keeps one.
+// Two blocks per wave where the registers allow it: one output strip, no
+// cos source, and at most 5 matrices (3 when X or Y need the per-element
+// paths).  Measured at 2^20 rows: image-like net (in 32, 2 hidden layers,
+// sigmoid out 3) 110 -> 95 us, 5 matrices 181.5 -> 166 us.
 template <int L, int OS, int ACT, bool VEC>
 constexpr int trainw_nt() {
-  return (ACT != ACT_SINE && OS == 1 && L <= (VEC ? 4 : 3)) ? 2 : 1;
+  return (ACT != ACT_SINE && OS == 1 && L <= (VEC ? 5 : 3)) ? 2 : 1;
 }
 
 template <int L, int OS, int ACT, bool VEC>
@@ -348,7 +347,7 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
     // at the start of the tile); then the next tile's X and T into the
     // buffers the forward no longer needs.
     u32x4 xc[NT][KBW];
-    {
+    auto load_xc = [&]() {
       const rsrc_t xr = make_rsrc(a.X + r.row0 * in_dim, r.vr * in_dim * 2);
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
@@ -375,8 +374,7 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
         for (int kb = 0; kb < KBW; ++kb)
           xc[n][kb] = u32x4{h[2 * kb][0], h[2 * kb][1], h[2 * kb + 1][0], h[2 * kb + 1][1]};
       }
-    }
-    if (tile + G < a.ntiles) load_xt(tile + G);
+    };
 
     // Layer l.  Phase 1: D_{l+1} (in `cur`) and A_l (this wave's rows)
     // transposed into DT and AT.  Phase 2 (after a barrier): the wave's G_l
@@ -386,6 +384,16 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
     auto layer_step = [&](auto lc, const u32x4 (&cur)[NT][KBW], u32x4 (&nxt)[NT][KBW]) {
       constexpr int l = decltype(lc)::value;
       constexpr int SD = Gm::sd(l);
+      // X in chain order for AT at layer 0 (from cache), then the next
+      // tile's X and T: requested as the backward starts, or for 5
+      // matrices one layer before they are needed, so that they do not hold
+      // registers through the deeper layers (which lets the 5-matrix net
+      // keep two blocks per wave: 181.5 -> 166 us at 2^20 rows; the shorter
+      // nets are 1-2% faster with the early request).
+      if constexpr (l == (L >= 5 ? 1 : L - 1)) {
+        load_xc();
+        if (tile + G < a.ntiles) load_xt(tile + G);
+      }
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
         static_for<0, SD>([&](auto sc) {
