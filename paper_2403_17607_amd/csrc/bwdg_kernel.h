@@ -39,7 +39,7 @@
 
 namespace ffmlp {
 
-template <int W, int L, int OS>
+template <int W, int L, int OS, bool XT8 = false>
 struct BwdgGeom {
   static constexpr int NW = kBwdgWaves, SW = W / 16, KBW = (W + 31) / 32;
   static constexpr int KBO = (OS * 16 + 31) / 32;  // k-blocks of the output delta
@@ -47,7 +47,18 @@ struct BwdgGeom {
   // Resident fragments: backward layers 1 .. L-2 whole, then the output
   // layer's first KBO k-blocks of each strip (past out_dim they are zero).
   static constexpr int WFRAGS = (L - 2) * SW * KBW + SW * KBO;
-  static constexpr size_t lds_bytes() { return (size_t)WFRAGS * 1024 + (size_t)W * LDT * 2; }
+  // XT, the tile's X transposed for G_0: at width 128 with 3 or more
+  // matrices it takes the place of layer 1's weights (32 KiB, exactly one
+  // hidden layer; LDS holds nothing else that size), which are not read
+  // during layer 0 and are staged again for the next tile; otherwise it has
+  // its own space after DT.
+  // Only with XT8 (in_dim a multiple of 8); otherwise each wave loads its X
+  // strip of the tile's rows as it loads the stash strips.
+  static constexpr bool XT_REUSE = XT8 && W == 128 && L >= 3;
+  static constexpr size_t xt_off() { return XT_REUSE ? 0 : (size_t)WFRAGS * 1024 + (size_t)W * LDT * 2; }
+  static constexpr size_t lds_bytes() {
+    return (size_t)WFRAGS * 1024 + (size_t)W * LDT * 2 + ((XT8 && !XT_REUSE) ? (size_t)W * LDT * 2 : 0);
+  }
   static constexpr int woff(int l) { return (l - 1) * SW * KBW; }  // fragment offset, layer l >= 1
   // Slices of G_l: SW k-strips (features of A_l) x sd(l) j-strips (of
   // D_{l+1}) of 16x16 tiles; wave w owns tiles w tpw .. w tpw + tpw - 1
@@ -65,14 +76,15 @@ struct BwdgGeom {
   static_assert(L >= 2 && L <= kBwdgMaxL, "fused backward: 2 .. kBwdgMaxL matrices");
 };
 
-template <int W, int L, int OS, int SEEDED, int DER>
+template <int W, int L, int OS, int SEEDED, int DER, bool XT8>
 __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a) {
-  using Gm = BwdgGeom<W, L, OS>;
+  using Gm = BwdgGeom<W, L, OS, XT8>;
   constexpr int NW = Gm::NW, SW = Gm::SW, KBW = Gm::KBW, KBO = Gm::KBO, LDT = Gm::LDT;
   constexpr int NACC = Gm::nacc();
   constexpr int KS = kBwdgRows / 32;  // 32-row contraction steps per tile
   extern __shared__ u32x4 smem[];
   uint16_t* DT = reinterpret_cast<uint16_t*>(smem + (size_t)Gm::WFRAGS * 64);
+  uint16_t* XT = reinterpret_cast<uint16_t*>(reinterpret_cast<uint8_t*>(smem) + Gm::xt_off());
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // wave-uniform
   const int li = lane & 15, lg = lane >> 4;
@@ -168,13 +180,30 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
   };
 
   // A_l strip of the wave's G_l slice, rows tr0 .. tr0 + 127, lane (g, i)
-  // of block b holding row 16 b + i, features 16 kt + 4 g .. + 3.
+  // of block b holding row 16 b + i, features 16 kt + 4 g .. + 3 (l >= 1,
+  // from the stash).  For l = 0 with XT8 (in_dim a multiple of 8) instead
+  // the wave's own 16 rows of X, every feature, in input order (lane group
+  // g: features 32 kb + 8 g .. + 7 in ar[2 kb], ar[2 kb + 1]): whole rows are
+  // contiguous in X, so these loads use every byte of the lines they touch,
+  // where a 16-feature strip of 128 rows uses a quarter of each (measured:
+  // 38 us of the 2^20-row training step at width 128); the waves transpose
+  // them into XT for G_0.  Other input widths load the X strip.
   u32x2 ar[NW];
   auto load_a = [&](auto lc, const TileGeom& t) {
     constexpr int l = decltype(lc)::value;
-    int kt, jt0;
-    if (!slice(lc, kt, jt0)) return;
-    if constexpr (l == 0) {
+    if constexpr (l == 0 && XT8) {
+      static_assert(2 * KBW <= NW, "a wave's X rows fit the strip registers");
+      const rsrc_t xr = make_rsrc(a.X + t.row0 * in_dim, t.vrows * in_dim * 2);
+#pragma unroll
+      for (int kb = 0; kb < KBW; ++kb) {
+        const int f0 = 32 * kb + 8 * lg;
+        const u32x4 v = bload128(xr, f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB, 0u);
+        ar[2 * kb] = u32x2{v.x, v.y};
+        ar[2 * kb + 1] = u32x2{v.z, v.w};
+      }
+    } else if constexpr (l == 0) {
+      int kt, jt0;
+      if (!slice(lc, kt, jt0)) return;
       int64_t rows = M - t.tr0;
       rows = rows < 0 ? 0 : (rows > kBwdgRows ? kBwdgRows : rows);
       const rsrc_t xr = make_rsrc(a.X + t.tr0 * in_dim, rows * in_dim * 2);
@@ -198,6 +227,8 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
         }
       }
     } else {
+      int kt, jt0;
+      if (!slice(lc, kt, jt0)) return;
       const rsrc_t sr = make_rsrc(a.stashA + (size_t)(l - 1) * a.M16 * W + (size_t)t.tr0 * W,
                                   (int64_t)t.tvblk * 32 * W);
 #pragma unroll
@@ -327,7 +358,28 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
         *reinterpret_cast<u32x2*>(DT + dt_off(16 * s + li, 4 * (wave >> 1) + lg) +
                                   4 * ((wave & 1) ^ (lg & 1))) = v;
       });
-      __syncthreads();  // DT holds D_{l+1} of all 128 rows
+      if constexpr (l == 0 && XT8) {
+        // XT: this wave's rows of X transposed, in DT's layout.  The k-block
+        // kb operand holds features 32 kb + 8 g + q (q < 8) in lane group g,
+        // so sel0 (sel1) gives lane (g, n) feature 32 kb + 8 (n / 4) + n % 4
+        // (+ 4) of rows 4 g .. 4 g + 3.
+#pragma unroll
+        for (int kb = 0; kb < KBW; ++kb) {
+          const u32x4 src = {ar[2 * kb].x, ar[2 * kb].y, ar[2 * kb + 1].x, ar[2 * kb + 1].y};
+#pragma unroll
+          for (int h = 0; h < 2; ++h) {
+            const f32x4 o = mfma16(src, h ? sel1 : sel0, zero4);
+            const int f = 32 * kb + 8 * (li >> 2) + 4 * h + (li & 3);
+            *reinterpret_cast<u32x2*>(XT + dt_off(f, 4 * (wave >> 1) + lg) + 4 * ((wave & 1) ^ (lg & 1))) =
+                u32x2{pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
+          }
+        }
+      }
+      // DT (and at layer 0 XT) hold all 128 rows.  Before layer 1 the wave
+      // also waits for its share of layer 1's weights, staged again after
+      // the previous tile's layer 0 when XT used their space.
+      if constexpr (Gm::XT_REUSE && l == 1) drain_and_sync();
+      else __syncthreads();
 
       int kt, jt0;
       const bool has = slice(lc, kt, jt0);
@@ -336,7 +388,12 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
       // (g, n), the order the DT writes above used (odd lane groups hold
       // block 2 ks + 1 in slots 0-3, see dt_off)
       u32x4 aop[KS];
-      if (has) {
+      if (XT8 && has && l == 0) {
+        // X strip kt of the tile's rows from XT, in DT's row order
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks)
+          aop[ks] = *reinterpret_cast<const u32x4*>(XT + dt_off(16 * kt + li, 4 * ks + lg));
+      } else if (has) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
           const u32x4 src = {ar[2 * ks].x, ar[2 * ks].y, ar[2 * ks + 1].x, ar[2 * ks + 1].y};
@@ -408,7 +465,12 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
         if constexpr (DER == 0) mw = load_mask(l - 2, t);
         else load_der(l - 2, t, sv);
       }
-      __syncthreads();  // every wave is done reading DT
+      __syncthreads();  // every wave is done reading DT (and XT)
+      if constexpr (Gm::XT_REUSE && l == 0) {
+        // XT's space back to layer 1's weights for the next tile (waited
+        // for before that tile's layer 1)
+        if (more) stage_frags(smem + (size_t)Gm::woff(1) * 64, a.packed, (uint32_t)(SW * KBW), wave, NW, lane);
+      }
     };
 
     static_for<0, L>([&](auto ic) {
@@ -442,15 +504,15 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
   });
 }
 
-template <int W, int L, int OS, int SEEDED, int DER>
-static hipError_t bwdg_launch_t(const BwdgArgs& a, hipStream_t stream, int* grid_out) {
-  using Gm = BwdgGeom<W, L, OS>;
+template <int W, int L, int OS, int SEEDED, int DER, bool XT8>
+static hipError_t bwdg_launch_t1(const BwdgArgs& a, hipStream_t stream, int* grid_out) {
+  using Gm = BwdgGeom<W, L, OS, XT8>;
   DeviceInfo di;
   hipError_t e = device_info(&di);
   if (e != hipSuccess) return e;
   const size_t lds = Gm::lds_bytes();
   if (lds > (size_t)di.max_lds) return hipErrorNotSupported;
-  auto kern = bwdg_kernel<W, L, OS, SEEDED, DER>;
+  auto kern = bwdg_kernel<W, L, OS, SEEDED, DER, XT8>;
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), kBwdgWaves * 64, lds, &occ);
   if (e != hipSuccess) return e;
@@ -461,6 +523,13 @@ static hipError_t bwdg_launch_t(const BwdgArgs& a, hipStream_t stream, int* grid
   *grid_out = grid;
   hipLaunchKernelGGL(kern, dim3(grid), dim3(kBwdgWaves * 64), lds, stream, a);
   return hipGetLastError();
+}
+
+// XT8: the X tile exchanged through LDS for G_0 (in_dim a multiple of 8).
+template <int W, int L, int OS, int SEEDED, int DER>
+static hipError_t bwdg_launch_t(const BwdgArgs& a, hipStream_t stream, int* grid_out) {
+  if (a.in_dim % 8 == 0) return bwdg_launch_t1<W, L, OS, SEEDED, DER, true>(a, stream, grid_out);
+  return bwdg_launch_t1<W, L, OS, SEEDED, DER, false>(a, stream, grid_out);
 }
 
 template <int W, int OS, int DER>
