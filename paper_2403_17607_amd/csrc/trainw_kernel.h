@@ -82,7 +82,6 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
   const int64_t M = a.M;
   const int in_dim = a.in_dim, out_dim = a.out_dim, out_act = a.out_act;
   const int SO = (out_dim + 15) >> 4;
-  const int SI = (in_dim + 15) >> 4;  // strips of X
   const bool xvec = VEC || (in_dim & 7) == 0;
   const bool yvec = VEC || (out_dim & 3) == 0;
 
@@ -342,37 +341,31 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
       default: output_layer(std::integral_constant<int, ACT_LINEAR>{}); break;
     }
 
-    // ---- backward.  X of the wave's rows once more, in chain order (the
-    // transposes for AT want it so; from cache: the wave read these bytes
-    // at the start of the tile); then the next tile's X and T into the
-    // buffers the forward no longer needs.
+    // ---- backward.  X of the wave's rows once more for AT (from cache: the
+    // wave read these bytes at the start of the tile); then the next tile's
+    // X and T into the buffers the forward no longer needs.
     u32x4 xc[NT][KBW];
     auto load_xc = [&]() {
+      // input order, as for the forward (lane group g of block n: features
+      // 32 kb + 8 g .. + 7): 16 or 8 contiguous bytes per lane and row
       const rsrc_t xr = make_rsrc(a.X + r.row0 * in_dim, r.vr * in_dim * 2);
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
         const uint32_t so = (uint32_t)(n * 32 * in_dim);
-        uint32_t h[SW][2];
 #pragma unroll
-        for (int s = 0; s < SW; ++s) {
-          const int f0 = 16 * s + 4 * lg;
-          if (VEC || (in_dim & 3) == 0) {
-            const uint32_t voff = f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB;
-            const u32x2 v = bload64(xr, voff, so);
-            h[s][0] = v.x;
-            h[s][1] = v.y;
+        for (int kb = 0; kb < KBW; ++kb) {
+          const int f0 = 32 * kb + 8 * lg;
+          if (xvec) {
+            xc[n][kb] = bload128(xr, f0 < in_dim ? (uint32_t)((li * in_dim + f0) * 2) : kOOB, so);
           } else {
-            uint32_t e[4];
+            uint32_t e[8];
 #pragma unroll
-            for (int q = 0; q < 4; ++q)
+            for (int q = 0; q < 8; ++q)
               e[q] = bload16(xr, f0 + q < in_dim ? (uint32_t)((li * in_dim + f0 + q) * 2) : kOOB, so);
-            h[s][0] = e[0] | (e[1] << 16);
-            h[s][1] = e[2] | (e[3] << 16);
+            xc[n][kb] = u32x4{e[0] | (e[1] << 16), e[2] | (e[3] << 16), e[4] | (e[5] << 16),
+                              e[6] | (e[7] << 16)};
           }
         }
-#pragma unroll
-        for (int kb = 0; kb < KBW; ++kb)
-          xc[n][kb] = u32x4{h[2 * kb][0], h[2 * kb][1], h[2 * kb + 1][0], h[2 * kb + 1][1]};
       }
     };
 
@@ -403,7 +396,11 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
         static_for<0, SW>([&](auto sc) {
           constexpr int s = decltype(sc)::value;
           if constexpr (l == 0) {
-            if (s < SI) put_t(AT, 16 * s + li, n, mfma16(xc[n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+            // X in input order: k-block s / 2, half s % 2 gives lane (g, n)
+            // feature 32 (s / 2) + 8 (n / 4) + 4 (s % 2) + n % 4
+            if (32 * (s >> 1) < in_dim)
+              put_t(AT, 32 * (s >> 1) + 8 * (li >> 2) + 4 * (s & 1) + (li & 3), n,
+                    mfma16(xc[n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
           } else {
             put_t(AT, 16 * s + li, n, mfma16(ach[l - 1][n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
           }
