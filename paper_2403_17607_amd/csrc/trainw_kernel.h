@@ -377,15 +377,17 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
     auto layer_step = [&](auto lc, const u32x4 (&cur)[NT][KBW], u32x4 (&nxt)[NT][KBW]) {
       constexpr int l = decltype(lc)::value;
       constexpr int SD = Gm::sd(l);
-      // X in chain order for AT at layer 0 (from cache), then the next
-      // tile's X and T: requested as the backward starts, or for 5
-      // matrices one layer before they are needed, so that they do not hold
-      // registers through the deeper layers (which lets the 5-matrix net
-      // keep two blocks per wave: 181.5 -> 166 us at 2^20 rows; the shorter
-      // nets are 1-2% faster with the early request).
+      // X for AT at layer 0 (from cache), then the next tile's X and T:
+      // requested as the backward starts, or for 5 matrices one layer before
+      // they are needed, so that they do not hold registers through the
+      // deeper layers (which lets the 5-matrix net keep two blocks per wave:
+      // 181.5 -> 166 us at 2^20 rows; the shorter nets are 1-2% faster with
+      // the early request).  For 5 matrices the next tile's inputs go out
+      // after layer 1's first barrier: requested before its transposes, a
+      // register reload there waited for them (169 -> 162 us).
       if constexpr (l == (L >= 5 ? 1 : L - 1)) {
         load_xc();
-        if (tile + G < a.ntiles) load_xt(tile + G);
+        if constexpr (L < 5) { if (tile + G < a.ntiles) load_xt(tile + G); }
       }
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
@@ -407,6 +409,7 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
         });
       }
       __syncthreads();  // DT and AT hold the tile's rows
+      if constexpr (L >= 5 && l == 1) { if (tile + G < a.ntiles) load_xt(tile + G); }
 
       int kt, jt0;
       const bool has = slice(lc, kt, jt0);
