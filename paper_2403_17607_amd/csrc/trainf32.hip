@@ -11,8 +11,9 @@ hipError_t launch_train_fused_w(int L, int act, int out_dim, const TrainfArgs& a
 template <>
 hipError_t launch_train_fused_w<32>(int L, int act, int out_dim, const TrainfArgs& a, hipStream_t s,
                                     int* grid_out) {
-  (void)out_dim;
-  return trainf_by_act<32, 2>(act, L, a, s, grid_out);
+  // one output strip when it suffices: no G or T work on a padding strip
+  // (2^20 rows, out 16: 53.0 -> 51.9 us)
+  return out_dim <= 16 ? trainf_by_act<32, 1>(act, L, a, s, grid_out) : trainf_by_act<32, 2>(act, L, a, s, grid_out);
 }
 
 }  // namespace ffmlp

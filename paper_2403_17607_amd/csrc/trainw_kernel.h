@@ -384,10 +384,13 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
       // 181.5 -> 166 us at 2^20 rows; the shorter nets are 1-2% faster with
       // the early request).  For 5 matrices the next tile's inputs go out
       // after layer 1's first barrier: requested before its transposes, a
-      // register reload there waited for them (169 -> 162 us).
+      // register reload there waited for them (169 -> 162 us).  The next
+      // tile's request is made after the last tile too (rows past M read
+      // as 0), so the wait for X before layer 0 counts it instead of
+      // draining it.
       if constexpr (l == (L >= 5 ? 1 : L - 1)) {
         load_xc();
-        if constexpr (L < 5) { if (tile + G < a.ntiles) load_xt(tile + G); }
+        if constexpr (L < 5) load_xt(tile + G);
       }
 #pragma unroll
       for (int n = 0; n < NT; ++n) {
@@ -409,7 +412,7 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
         });
       }
       __syncthreads();  // DT and AT hold the tile's rows
-      if constexpr (L >= 5 && l == 1) { if (tile + G < a.ntiles) load_xt(tile + G); }
+      if constexpr (L >= 5 && l == 1) load_xt(tile + G);
 
       int kt, jt0;
       const bool has = slice(lc, kt, jt0);
