@@ -150,6 +150,17 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
     const u32x2 v = {pack_bf16x2(o[0], o[1]), pack_bf16x2(o[2], o[3])};
     *reinterpret_cast<u32x2*>(tile + dt_off(f, 4 * (b >> 1) + lg) + 4 * ((b & 1) ^ (lg & 1))) = v;
   };
+  // With two blocks per wave the chunk 4 w + g of feature f holds rows
+  // 4 g .. 4 g + 3 of both of wave w's blocks (block 2 w in its first half),
+  // written as one 16-byte store: eight lanes of one lane group then cover
+  // eight different chunks, free of bank conflicts, where the 8-byte stores
+  // of sixteen lanes met two to a bank (the stores took half of the
+  // kernel's LDS cycles, half of them conflict stalls).
+  auto put_t2 = [&](uint16_t* tile, int f, const f32x4& o0, const f32x4& o1) {
+    const u32x4 v = {pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3]), pack_bf16x2(o1[0], o1[1]),
+                     pack_bf16x2(o1[2], o1[3])};
+    *reinterpret_cast<u32x4*>(tile + dt_off(f, 4 * wave + lg)) = v;
+  };
 
   drain_and_sync();  // weights in LDS
 
@@ -392,24 +403,44 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
         load_xc();
         if constexpr (L < 5) load_xt(tile + G);
       }
-#pragma unroll
-      for (int n = 0; n < NT; ++n) {
+      if constexpr (NT == 2) {
         static_for<0, SD>([&](auto sc) {
           constexpr int s = decltype(sc)::value;
-          put_t(DT, 16 * s + li, n, mfma16(cur[n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+          const u32x4 sl = (s & 1) ? sel1 : sel0;
+          put_t2(DT, 16 * s + li, mfma16(cur[0][s >> 1], sl, zero4), mfma16(cur[1][s >> 1], sl, zero4));
         });
         static_for<0, SW>([&](auto sc) {
           constexpr int s = decltype(sc)::value;
+          const u32x4 sl = (s & 1) ? sel1 : sel0;
           if constexpr (l == 0) {
             // X in input order: k-block s / 2, half s % 2 gives lane (g, n)
             // feature 32 (s / 2) + 8 (n / 4) + 4 (s % 2) + n % 4
             if (32 * (s >> 1) < in_dim)
-              put_t(AT, 32 * (s >> 1) + 8 * (li >> 2) + 4 * (s & 1) + (li & 3), n,
-                    mfma16(xc[n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+              put_t2(AT, 32 * (s >> 1) + 8 * (li >> 2) + 4 * (s & 1) + (li & 3),
+                     mfma16(xc[0][s >> 1], sl, zero4), mfma16(xc[1][s >> 1], sl, zero4));
           } else {
-            put_t(AT, 16 * s + li, n, mfma16(ach[l - 1][n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+            put_t2(AT, 16 * s + li, mfma16(ach[l - 1][0][s >> 1], sl, zero4),
+                   mfma16(ach[l - 1][1][s >> 1], sl, zero4));
           }
         });
+      } else {
+#pragma unroll
+        for (int n = 0; n < NT; ++n) {
+          static_for<0, SD>([&](auto sc) {
+            constexpr int s = decltype(sc)::value;
+            put_t(DT, 16 * s + li, n, mfma16(cur[n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+          });
+          static_for<0, SW>([&](auto sc) {
+            constexpr int s = decltype(sc)::value;
+            if constexpr (l == 0) {
+              if (32 * (s >> 1) < in_dim)
+                put_t(AT, 32 * (s >> 1) + 8 * (li >> 2) + 4 * (s & 1) + (li & 3), n,
+                      mfma16(xc[n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+            } else {
+              put_t(AT, 16 * s + li, n, mfma16(ach[l - 1][n][s >> 1], (s & 1) ? sel1 : sel0, zero4));
+            }
+          });
+        }
       }
       __syncthreads();  // DT and AT hold the tile's rows
       if constexpr (L >= 5 && l == 1) load_xt(tile + G);
