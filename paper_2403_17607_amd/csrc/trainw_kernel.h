@@ -137,9 +137,11 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainw_kernel(const TrainfA
     }
   };
   // Element offset of chunk c (8 rows, one 16-byte operand) of feature row f
-  // in DT or AT; chunk c is stored at c ^ (f % 16), which keeps the 16-byte
-  // reads and the 8-byte writes free of bank conflicts.
-  auto dt_off = [&](int f, int c) { return f * LDT + ((c ^ (f & 15)) << 3); };
+  // in DT or AT; chunk c is stored at c ^ (f % 16) ^ 4 [f / 8 odd]: eight
+  // consecutive features then use eight different bank groups, and so do
+  // the features 8 (n / 4) + n % 4 that the input-order X transposes store
+  // (with f % 16 alone, features f and f + 8 met there).
+  auto dt_off = [&](int f, int c) { return f * LDT + ((c ^ (f & 15) ^ ((f >> 1) & 4)) << 3); };
   // Rows 4 g .. 4 g + 3 of the tile's block b (block n of wave w is
   // b = w NT + n), one feature per lane, go to chunk 4 (b / 2) + g, half
   // (b % 2) ^ (g % 2): the order in which the 16-byte reads below hand 8
