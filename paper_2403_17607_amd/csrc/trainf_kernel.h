@@ -347,15 +347,36 @@ __global__ __launch_bounds__(kTrainfWaves * 64) void trainf_kernel(const TrainfA
           dop[j] = u32x4{pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3]),
                          pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
         }
+        if constexpr (SW == 2) {
+          // Width 32: each block's two strips are already one operand (the
+          // forward's k-block); sel0 / sel1 transpose its strip 0 / 1.  No
+          // operand is assembled from the two blocks' strips (4 register
+          // moves per transpose pair).
+          f32x4 o[2][2];
 #pragma unroll
-        for (int t = 0; t < SW; ++t) {
-          const u32x4 src = {ar[2 * k][t].x, ar[2 * k][t].y, ar[2 * k + 1][t].x, ar[2 * k + 1][t].y};
-          const f32x4 o0 = mfma16(src, sel0, zero4);
-          const f32x4 o1 = mfma16(src, sel1, zero4);
-          const u32x4 aop = {pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3]),
-                             pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
+          for (int b = 0; b < 2; ++b) {
+            const u32x4 src = {ar[2 * k + b][0].x, ar[2 * k + b][0].y, ar[2 * k + b][1].x, ar[2 * k + b][1].y};
+            o[b][0] = mfma16(src, sel0, zero4);
+            o[b][1] = mfma16(src, sel1, zero4);
+          }
 #pragma unroll
-          for (int j = 0; j < SD; ++j) gacc[GO + t * SD + j] = mfma16(aop, dop[j], gacc[GO + t * SD + j]);
+          for (int t = 0; t < 2; ++t) {
+            const u32x4 aop = {pack_bf16x2(o[0][t][0], o[0][t][1]), pack_bf16x2(o[0][t][2], o[0][t][3]),
+                               pack_bf16x2(o[1][t][0], o[1][t][1]), pack_bf16x2(o[1][t][2], o[1][t][3])};
+#pragma unroll
+            for (int j = 0; j < SD; ++j) gacc[GO + t * SD + j] = mfma16(aop, dop[j], gacc[GO + t * SD + j]);
+          }
+        } else {
+#pragma unroll
+          for (int t = 0; t < SW; ++t) {
+            const u32x4 src = {ar[2 * k][t].x, ar[2 * k][t].y, ar[2 * k + 1][t].x, ar[2 * k + 1][t].y};
+            const f32x4 o0 = mfma16(src, sel0, zero4);
+            const f32x4 o1 = mfma16(src, sel1, zero4);
+            const u32x4 aop = {pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3]),
+                               pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])};
+#pragma unroll
+            for (int j = 0; j < SD; ++j) gacc[GO + t * SD + j] = mfma16(aop, dop[j], gacc[GO + t * SD + j]);
+          }
         }
       }
       if constexpr (l >= 1) {
