@@ -140,7 +140,15 @@ def _require(t, name: str, dtype, shape=None, min_numel=None, device=None) -> No
         raise ValueError(f"{name} is on {t.device}, the other arguments on {device}")
 
 
+_raw_stream = getattr(torch._C, "_cuda_getCurrentRawStream", None)
+
+
 def _stream(device) -> int:
+    """The current HIP stream of `device` as an integer handle.  torch's
+    raw accessor takes about 0.2 us where current_stream() takes 2, which
+    matters for small batches, whose kernels run for a few microseconds."""
+    if _raw_stream is not None and device.index is not None:
+        return _raw_stream(device.index)
     return torch.cuda.current_stream(device).cuda_stream
 
 
