@@ -298,9 +298,11 @@ def roofline_plot(path, points, batch):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--steps", type=int, default=None,
+                    help="timed steps K per repeat (default: the paper's protocol, "
+                         "max(1000 * 2^18 / batch, 250))")
     ap.add_argument("--warmup", type=int, default=10)
-    ap.add_argument("--repeats", type=int, default=1,
+    ap.add_argument("--repeats", type=int, default=5,
                     help="time the K steps this many times and report the median repeat "
                          "(with the min-max spread)")
     ap.add_argument("--width", type=int, default=128)
@@ -326,7 +328,9 @@ def main():
               "one all-reduce of the gradients).", file=sys.stderr)
         sys.exit(2)
 
-    K, Wm, R, M = args.steps, args.warmup, args.repeats, args.batch
+    M = args.batch
+    K = args.steps if args.steps is not None else max(1000 * (1 << 18) // max(M, 1), 250)
+    Wm, R = args.warmup, args.repeats
     if args.roofline_plot:
         points = []
         for w in (16, 32, 64, 128):
