@@ -201,7 +201,7 @@ int run_reduce(const mlp* h, const WsLayout& w, uint8_t* ws, int64_t M, int P, f
 // Returns 1 (nothing enqueued) when the fused kernel does not cover the net.
 int run_fused_backward(const mlp* h, const void* packed, const uint16_t* X, const float* dY,
                        const WsLayout& w, uint8_t* ws, int64_t M, float* G, float* loss, int nloss,
-                       int seeded, bool masks, hipStream_t s) {
+                       int seeded, bool masks, hipStream_t s, bool stash_t = false) {
   if (M <= 0 || !backward_fused_supported(h->width, n_mats(h), h->act, h->in_dim, h->out_dim))
     return 1;
   const PackGeom g = pack_geom(h);
@@ -225,6 +225,7 @@ int run_fused_backward(const mlp* h, const void* packed, const uint16_t* X, cons
   a.out_act = h->out_act;
   a.ntiles = (int)((M + kBwdgRows - 1) / kBwdgRows);
   a.layH_frags = g.bwd_hidden;
+  a.stash_t = stash_t ? 1 : 0;
   int P = 0;
   hipError_t e = launch_backward_fused(h->width, n_mats(h), h->out_dim, seeded, a, s, &P);
   if (e == hipErrorNotSupported) return 1;
@@ -637,13 +638,19 @@ int train_step_impl(const mlp_t* h, const void* packed, const uint16_t* X, const
                        backward_fused_supported(h->width, n_mats(h), h->act, h->in_dim, h->out_dim);
     const bool masks = h->act == MLP_ACT_RELU && !(fused && h->width <= 64);
     a.reluMask = masks ? reinterpret_cast<uint32_t*>(ws + w.reluMask) : nullptr;
+    // At width 128 the fused backward takes the activations transposed
+    // (the forward has matrix-core time to spare, the backward does not).
+    const bool stash_t = fused && h->width == 128 && masks;
+    a.stash_t = stash_t ? 1 : 0;
     a.deltaOut = reinterpret_cast<uint16_t*>(ws + w.deltaOut);
     a.lossPart = reinterpret_cast<float*>(ws + w.lossPart);
     hipError_t e = launch_forward(h->width, h->act, FWD_TRAIN, a, s, &nloss);
     if (e != hipSuccess) return hip_fail(e, "forward kernel launch");
     if (n_mats(h) > 1) {
-      const int rc = run_fused_backward(h, packed, X, nullptr, w, ws, M, G, loss, nloss, 0, masks, s);
+      const int rc = run_fused_backward(h, packed, X, nullptr, w, ws, M, G, loss, nloss, 0, masks, s, stash_t);
       if (rc <= 0) return rc;
+      if (stash_t)  // no other backward reads the transposed stash
+        return fail(MLP_ERR_UNSUPPORTED, "fused backward kernel unavailable on this device");
       if (h->act == MLP_ACT_RELU && !masks)  // the unfused backward needs the masks
         return fail(MLP_ERR_UNSUPPORTED, "fused backward kernel unavailable on this device");
       BwdArgs b = bwd_args(h, packed, w, ws, M);

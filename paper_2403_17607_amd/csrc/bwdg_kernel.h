@@ -76,7 +76,10 @@ struct BwdgGeom {
   static_assert(L >= 2 && L <= kBwdgMaxL, "fused backward: 2 .. kBwdgMaxL matrices");
 };
 
-template <int W, int L, int OS, int SEEDED, int DER, bool XT8>
+// TST: stashA written transposed by the training forward (each 16-row
+// block's strip s as lane (g, n) = feature 16 s + n of rows 4 g .. 4 g + 3),
+// so the A operand of G_l is loaded as it is, with no transposes here.
+template <int W, int L, int OS, int SEEDED, int DER, bool XT8, bool TST = false>
 __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a) {
   using Gm = BwdgGeom<W, L, OS, XT8>;
   constexpr int NW = Gm::NW, SW = Gm::SW, KBW = Gm::KBW, KBO = Gm::KBO, LDT = Gm::LDT;
@@ -231,8 +234,21 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
       if (!slice(lc, kt, jt0)) return;
       const rsrc_t sr = make_rsrc(a.stashA + (size_t)(l - 1) * a.M16 * W + (size_t)t.tr0 * W,
                                   (int64_t)t.tvblk * 32 * W);
+      if constexpr (TST) {
+        // block pair (2 ks, 2 ks + 1) into ar[2 ks], ar[2 ks + 1] in the
+        // order of the operand below: odd lane groups take block 2 ks + 1
+        // first (the per-lane offset picks the block; no register moves)
+        const uint32_t sw = (uint32_t)(lg & 1) * SW * 512;
 #pragma unroll
-      for (int b = 0; b < NW; ++b) ar[b] = bload64(sr, lane * 8, (uint32_t)((b * SW + kt) * 512));
+        for (int ks = 0; ks < NW / 2; ++ks) {
+          const uint32_t so = (uint32_t)((2 * ks * SW + kt) * 512);
+          ar[2 * ks] = bload64(sr, lane * 8 + sw, so);
+          ar[2 * ks + 1] = bload64(sr, lane * 8 + (SW * 512 - sw), so);
+        }
+      } else {
+#pragma unroll
+        for (int b = 0; b < NW; ++b) ar[b] = bload64(sr, lane * 8, (uint32_t)((b * SW + kt) * 512));
+      }
     }
   };
   auto load_mask = [&](int idx, const TileGeom& t) -> uint32_t {
@@ -393,6 +409,9 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks)
           aop[ks] = *reinterpret_cast<const u32x4*>(XT + dt_off(16 * kt + li, 4 * ks + lg));
+      } else if (TST && l >= 1 && has) {  // X for G_0 keeps the transposes
+#pragma unroll
+        for (int ks = 0; ks < KS; ++ks) aop[ks] = u32x4{ar[2 * ks].x, ar[2 * ks].y, ar[2 * ks + 1].x, ar[2 * ks + 1].y};
       } else if (has) {
 #pragma unroll
         for (int ks = 0; ks < KS; ++ks) {
@@ -504,7 +523,7 @@ __global__ __launch_bounds__(kBwdgWaves * 64) void bwdg_kernel(const BwdgArgs a)
   });
 }
 
-template <int W, int L, int OS, int SEEDED, int DER, bool XT8>
+template <int W, int L, int OS, int SEEDED, int DER, bool XT8, bool TST = false>
 static hipError_t bwdg_launch_t1(const BwdgArgs& a, hipStream_t stream, int* grid_out) {
   using Gm = BwdgGeom<W, L, OS, XT8>;
   DeviceInfo di;
@@ -512,7 +531,7 @@ static hipError_t bwdg_launch_t1(const BwdgArgs& a, hipStream_t stream, int* gri
   if (e != hipSuccess) return e;
   const size_t lds = Gm::lds_bytes();
   if (lds > (size_t)di.max_lds) return hipErrorNotSupported;
-  auto kern = bwdg_kernel<W, L, OS, SEEDED, DER, XT8>;
+  auto kern = bwdg_kernel<W, L, OS, SEEDED, DER, XT8, TST>;
   int occ = 0;
   e = kernel_occupancy(reinterpret_cast<const void*>(kern), kBwdgWaves * 64, lds, &occ);
   if (e != hipSuccess) return e;
@@ -528,6 +547,14 @@ static hipError_t bwdg_launch_t1(const BwdgArgs& a, hipStream_t stream, int* gri
 // XT8: the X tile exchanged through LDS for G_0 (in_dim a multiple of 8).
 template <int W, int L, int OS, int SEEDED, int DER>
 static hipError_t bwdg_launch_t(const BwdgArgs& a, hipStream_t stream, int* grid_out) {
+  if (a.stash_t) {
+    // the transposed stash exists only for the training step at width 128
+    if constexpr (W == 128 && SEEDED == 0 && DER == 0) {
+      if (a.in_dim % 8 == 0) return bwdg_launch_t1<W, L, OS, SEEDED, DER, true, true>(a, stream, grid_out);
+      return bwdg_launch_t1<W, L, OS, SEEDED, DER, false, true>(a, stream, grid_out);
+    }
+    return hipErrorInvalidValue;
+  }
   if (a.in_dim % 8 == 0) return bwdg_launch_t1<W, L, OS, SEEDED, DER, true>(a, stream, grid_out);
   return bwdg_launch_t1<W, L, OS, SEEDED, DER, false>(a, stream, grid_out);
 }

@@ -112,6 +112,8 @@ struct FwdArgs {
   float scale;          // 2 / (M out_dim)
   int ntiles, resident;
   uint32_t lay0_frags, layH_frags, total_frags;  // 1 KiB fragment counts
+  int stash_t;          // training forward at width 128 for the fused backward:
+                        // stashA holds each strip transposed (see fwd_kernel.h)
 };
 
 struct BwdArgs {
@@ -152,6 +154,7 @@ struct BwdgArgs {
   int in_dim, out_dim, act, out_act;
   int ntiles;                // kBwdgRows-row tiles
   uint32_t layH_frags;       // 1 KiB fragments of one packed hidden layer
+  int stash_t;               // stashA written transposed (FwdArgs::stash_t)
 };
 
 // Fused training step (trainf_kernel): the forward pass, the loss, the

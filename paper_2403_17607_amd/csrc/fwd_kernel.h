@@ -77,7 +77,15 @@ constexpr int fwd_nt() {
   return TileCfg<W>::NT;
 }
 
-template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false, bool LIN = false>
+// TST (training forward at width 128, for the fused backward): each
+// 512-byte strip of a block in stashA holds the strip transposed, lane
+// (g, n) feature 16 s + n of rows 4 g .. 4 g + 3, instead of lane (g, i)
+// row i of features 16 s + 4 g .. + 3.  The fused backward reads it as the
+// A operand of G_l directly; otherwise it transposes every strip on the
+// matrix cores itself (8 MFMAs and their conversions per layer and wave,
+// on its critical path), where the forward, bound by HBM, has them to
+// spare.  Same bytes, same addresses.
+template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false, bool LIN = false, bool TST = false>
 __global__ __launch_bounds__((fwd_waves<W, MODE, SMALL, FU>() * 64)) void fwd_kernel(const FwdArgs a) {
   constexpr int NT = fwd_nt<W, MODE, SMALL, FU>(), NW = fwd_waves<W, MODE, SMALL, FU>();
   constexpr int KBW = (W + 31) / 32, SW = W / 16;
@@ -93,6 +101,25 @@ __global__ __launch_bounds__((fwd_waves<W, MODE, SMALL, FU>() * 64)) void fwd_ke
   const bool xvec = (in_dim & 7) == 0;
   const bool yvec = (out_dim & 3) == 0;
   const int out_act = LIN ? (int)ACT_LINEAR : a.out_act;
+  static_assert(!TST || (MODE == FWD_TRAIN && NT % 2 == 0), "transposed stash: training forward, block pairs");
+  // TST: 0/1 selection matrices; an MFMA of a block pair's strip (block n in
+  // slots 0-3, block n + 1 in slots 4-7) against sel0 (sel1) gives block n
+  // (n + 1) transposed, exactly.
+  u32x4 sel0 = {0u, 0u, 0u, 0u}, sel1 = {0u, 0u, 0u, 0u};
+  const f32x4 zero4 = {0.f, 0.f, 0.f, 0.f};
+  if constexpr (TST) {
+    const int q = li - 4 * lg;
+    if (q >= 0 && q < 4) {
+      const uint32_t one = 0x3F80u << (16 * (q & 1));
+      if (q < 2) {
+        sel0.x = one;
+        sel1.z = one;
+      } else {
+        sel0.y = one;
+        sel1.w = one;
+      }
+    }
+  }
   constexpr bool resident = RES;
   // Non-temporal stores, except for inference with streamed weights: there
   // every layer ends by waiting for all outstanding memory operations, the
@@ -277,6 +304,7 @@ __global__ __launch_bounds__((fwd_waves<W, MODE, SMALL, FU>() * 64)) void fwd_ke
         }
         f32x4 acc[NT];
         strip_product<NT, KBW>(afb[cur], in, acc);
+        u32x2 pq[TST ? NT : 1];
 #pragma unroll
         for (int n = 0; n < NT; ++n) {
           uint32_t p0, p1;
@@ -294,7 +322,9 @@ __global__ __launch_bounds__((fwd_waves<W, MODE, SMALL, FU>() * 64)) void fwd_ke
             mk[n] |= (nonzero_halves(p0) | (nonzero_halves(p1) << 1)) << (2 * s);
             pin(mk[n]);
           }
-          if constexpr (MODE != FWD_INFER) {
+          if constexpr (TST) {
+            pq[n] = u32x2{p0, p1};
+          } else if constexpr (MODE != FWD_INFER) {
             const uint32_t so = (uint32_t)((n * SW + s) * 512);
             bstore64<NTS>(u32x2{p0, p1}, sa, lane * 8, so);
             if constexpr (ACT == ACT_SINE) {
@@ -302,6 +332,19 @@ __global__ __launch_bounds__((fwd_waves<W, MODE, SMALL, FU>() * 64)) void fwd_ke
               const uint32_t c1 = pack_bf16x2(__cosf(acc[n][2]), __cosf(acc[n][3]));
               bstore64<NTS>(u32x2{c0, c1}, ss, lane * 8, so);
             }
+          }
+        }
+        if constexpr (TST) {
+          // the strip of blocks n, n + 1 transposed, each into its own 512
+          // bytes (rows past M are dropped by the range check as above)
+#pragma unroll
+          for (int n = 0; n < NT; n += 2) {
+            const u32x4 src = {pq[n].x, pq[n].y, pq[n + 1].x, pq[n + 1].y};
+            const f32x4 o0 = mfma16(src, sel0, zero4), o1 = mfma16(src, sel1, zero4);
+            bstore64<NTS>(u32x2{pack_bf16x2(o0[0], o0[1]), pack_bf16x2(o0[2], o0[3])}, sa, lane * 8,
+                          (uint32_t)((n * SW + s) * 512));
+            bstore64<NTS>(u32x2{pack_bf16x2(o1[0], o1[1]), pack_bf16x2(o1[2], o1[3])}, sa, lane * 8,
+                          (uint32_t)(((n + 1) * SW + s) * 512));
           }
         }
         // Keep each strip's work together: bounds the live registers.
@@ -544,10 +587,10 @@ struct FwdPick {
   int threads;
   int64_t rows;
 };
-template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false, bool LIN = false>
+template <int W, int ACT, int MODE, int FU, bool RES, bool SMALL = false, bool LIN = false, bool TST = false>
 static FwdPick fwd_pick() {
   constexpr int NW = fwd_waves<W, MODE, SMALL, FU>(), NT = fwd_nt<W, MODE, SMALL, FU>();
-  return FwdPick{fwd_kernel<W, ACT, MODE, FU, RES, SMALL, LIN>, NW * 64, (int64_t)NW * NT * 16};
+  return FwdPick{fwd_kernel<W, ACT, MODE, FU, RES, SMALL, LIN, TST>, NW * 64, (int64_t)NW * NT * 16};
 }
 
 // LIN: the output activation is linear (the common case) and fixed at
@@ -571,6 +614,13 @@ static hipError_t launch_t(const FwdArgs& a0, hipStream_t stream, int* grid_out)
   a.resident = res_bytes + (MODE == FWD_INFER ? 0 : 1024) <= (size_t)di.max_lds ? 1 : 0;
   const size_t lds = a.resident ? res_bytes : (size_t)2 * maxf * 1024;
   FwdPick pk = a.resident ? fwd_pick<W, ACT, MODE, 0, true, false, LIN>() : fwd_pick<W, ACT, MODE, 0, false, false, LIN>();
+  if constexpr (W == 128 && MODE == FWD_TRAIN) {
+    if (a.stash_t)
+      pk = a.resident ? fwd_pick<W, ACT, MODE, 0, true, false, LIN, true>()
+                      : fwd_pick<W, ACT, MODE, 0, false, false, LIN, true>();
+  } else {
+    if (a.stash_t) return hipErrorInvalidValue;  // only the width-128 training forward writes it
+  }
   if constexpr (MODE == FWD_INFER && W >= 64) {
     if (a.resident && a.L >= 2 && SO == 1 && (a.in_dim % 8) == 0)
       pk = (a.L & 1) ? fwd_pick<W, ACT, MODE, 1, true, false, LIN>() : fwd_pick<W, ACT, MODE, 2, true, false, LIN>();
