@@ -295,6 +295,12 @@ def roofline_plot(path, points, batch):
     plt.close(fig)
 
 
+def default_steps(M):
+    """Timed steps per repeat in the paper's protocol (section IV-A):
+    max(1000 * 2^18 / M, 250)."""
+    return max(1000 * (1 << 18) // max(M, 1), 250)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -329,7 +335,7 @@ def main():
         sys.exit(2)
 
     M = args.batch
-    K = args.steps if args.steps is not None else max(1000 * (1 << 18) // max(M, 1), 250)
+    K = args.steps if args.steps is not None else default_steps(M)
     Wm, R = args.warmup, args.repeats
     if args.roofline_plot:
         points = []

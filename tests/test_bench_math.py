@@ -73,3 +73,15 @@ def test_one_kernel_training_bytes_per_row():
         assert bench.train_bytes_per_row(w, d, 7, 3, "sine") == 14 + 12
     for w, d in [(16, 0), (16, 5), (32, 16), (64, 0), (64, 5), (128, 4)]:
         assert not bench.fused_step(w, d)
+
+
+def test_default_steps_paper_protocol():
+    """The bench's default step count follows section IV-A's rule,
+    max(1000 * 2^18 / M, 250): 250 at 2^20 rows and above, 1000 at 2^18,
+    4000 at 2^16."""
+    import bench
+    assert bench.default_steps(1 << 20) == 250
+    assert bench.default_steps(1 << 22) == 250
+    assert bench.default_steps(1 << 18) == 1000
+    assert bench.default_steps(1 << 16) == 4000
+    assert bench.default_steps(4096) == 64000
